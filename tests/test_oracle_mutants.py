@@ -1,0 +1,62 @@
+"""The oracle's pins must catch plausible mistakes.  Each case plants one
+mistake in a copy of the oracle's C source (on the CPU), builds it and runs
+the pin suite against that build in a subprocess: the suite has to fail."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "moe_oracle.c")
+PINS = os.path.join(ROOT, "tests", "test_oracle_pins.py")
+
+# (name, text to replace, replacement, which occurrence (0-based))
+MUTANTS = [
+    ("order_reversed", "return a > b;", "return a < b;", 0),
+    ("tie_to_higher_index", "return ia < ib;", "return ia > ib;", 1),
+    ("nan_first", "return b_nan;", "return a_nan;", 0),
+    ("gates_not_normalised", "exp((double)row[idx[j]] - m) / sum", "exp((double)row[idx[j]] - m)", 0),
+    ("gate_sign", "sum += exp((double)row[idx[j]] - m);", "sum += exp(m - (double)row[idx[j]]);", 0),
+    ("counts_transposed", "counts[(size_t)src[t] * E + e] += 1;", "counts[(size_t)e * S + src[t]] += 1;", 0),
+    ("load_counts_sources", "expert_load[e] += 1;", "expert_load[src[t]] += 1;", 0),
+    ("offsets_inclusive", "offsets[s + 1] = offsets[s] + (int32_t)fill[s];",
+     "offsets[s + 1] = offsets[s] + (int32_t)fill[s] + (s == 0);", 0),
+    ("unstable_within_slot", "int32_t r = offsets[s] + (int32_t)fill[s];",
+     "int32_t r = offsets[s + 1] - 1 - (int32_t)fill[s];", 0),
+    ("silu_sign", "return z / (1.0 + exp(-z));", "return z / (1.0 + exp(z));", 0),
+    ("silu_is_relu", "return z / (1.0 + exp(-z));", "return z > 0 ? z : 0.0;", 0),
+    ("gate_up_swapped", "h[i] = silu(g) * u;", "h[i] = silu(u) * g;", 0),
+    ("down_transposed", "acc += bf16_value(row[c]) * v[c];",
+     "acc += bf16_value(w[(size_t)c * n_out + (o % n_out)]) * v[c];", 0),
+    ("dropped_last_term", "for (int c = 0; c < n_in; ++c)", "for (int c = 0; c + 1 < n_in; ++c)", 0),
+    ("gate_weight_dropped", "o[c] += w[j] * y[c];", "o[c] += y[c];", 0),
+    ("remote_experts_kept", "if (s < 0)\n                continue;\n            rc = oracle_swiglu_ffn",
+     "if (s < 0)\n                s = idx[j] % E_local;\n            rc = oracle_swiglu_ffn", 0),
+    ("shared_dropped", "for (int q = 0; q < n_sh; ++q) {", "for (int q = 0; q < 0; ++q) {", 0),
+    ("combine_weight_dropped", "o[c] += w * bf16_value(", "o[c] += bf16_value(", 0),
+]
+
+
+def _mutate(src: str, old: str, new: str, nth: int) -> str:
+    pos = -1
+    for _ in range(nth + 1):
+        pos = src.find(old, pos + 1)
+        assert pos >= 0, f"pattern not found: {old!r}"
+    return src[:pos] + new + src[pos + len(old):]
+
+
+@pytest.mark.parametrize("name,old,new,nth", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_mutant(tmp_path, name, old, new, nth):
+    with open(SRC) as f:
+        src = f.read()
+    mutated = _mutate(src, old, new, nth)
+    assert mutated != src
+    c = tmp_path / "mutant.c"
+    c.write_text(mutated)
+    so = tmp_path / "libmutant.so"
+    subprocess.check_call(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", str(c), "-o", str(so), "-lm"])
+    env = dict(os.environ, MOE_ORACLE_LIB=str(so))
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider", PINS],
+                       cwd=ROOT, env=env, capture_output=True, text=True, timeout=300)
+    assert r.returncode == 1, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
