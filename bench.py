@@ -1,0 +1,276 @@
+#!/usr/bin/env python3
+"""Throughput of one GPU's MoE layer (route + source x expert counts +
+dispatch + SwiGLU expert FFN + combine) on MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--config NAME]
+
+A step is one moe_forward over one batch of the workload (default: the
+Mixtral-shaped decode step, 64 tokens, hidden 4096, 8 experts top-2,
+intermediate 14336), inputs and bf16 weights resident in HBM.  Prints one JSON
+line: whole-job tokens/s, per-stage kernel times measured live with HIP
+events on the launch stream, the roofline position of the dominant kernel and
+the CPU oracle's throughput on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "MoE-layer tokens/sec on 1 MI355X; expert-FFN % MFMA peak; route/permute % HBM BW"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, vendor figure
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, vendor figure
+STAGES = ("route", "permute", "ffn_up", "ffn_down", "combine")
+
+
+def parse_args(argv=None):
+    p = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--config", default="decode_mixtral")
+    p.add_argument("--seed", type=int, default=0)
+    p.add_argument("--cpu-seconds", type=float, default=15.0,
+                   help="budget of the CPU-oracle baseline sample")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--calib-copy-mib", type=int, default=0,
+                   help="also run a plain device copy of this size (HBM counter calibration)")
+    return p.parse_args(argv)
+
+
+class HipEvents:
+    """hipEvent_t handles from the HIP runtime the process already uses."""
+
+    def __init__(self, n: int):
+        import torch  # noqa: F401  (loads torch's HIP runtime first)
+        self.hip = ctypes.CDLL("libamdhip64.so.7")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.ev = []
+        for _ in range(n):
+            e = ctypes.c_void_p()
+            rc = self.hip.hipEventCreate(ctypes.byref(e))
+            if rc != 0:
+                raise RuntimeError(f"hipEventCreate failed ({rc})")
+            self.ev.append(e.value)
+
+    def elapsed_ms(self, a: int, b: int) -> float:
+        ms = ctypes.c_float()
+        rc = self.hip.hipEventElapsedTime(ctypes.byref(ms), self.ev[a], self.ev[b])
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return float(ms.value)
+
+    def close(self):
+        for e in self.ev:
+            self.hip.hipEventDestroy(e)
+
+
+def stage_work(cfg, R: int, active: int) -> dict:
+    """Algorithmic bytes and FLOPs of one launch of each stage (what the
+    method must move or compute: active experts' weights only, each tensor
+    read or written once)."""
+    T, H, E, k, I, S = cfg.T, cfg.H, cfg.E, cfg.k, cfg.I, cfg.S
+    n_sh, I_sh = cfg.n_shared, (cfg.I_shared if cfg.n_shared else 0)
+    bf = 2
+    w = {}
+    w["route"] = dict(bytes=T * E * 4 + T * 4 + T * k * 8 + 2 * S * E * 8, flops=0)
+    w["permute"] = dict(bytes=T * k * 4 + (cfg.E_local + 1) * 4 + R * 4 + T * k * 4 + 2 * R * H * bf,
+                        flops=0)
+    w["ffn_up"] = dict(bytes=active * 2 * I * H * bf + n_sh * 2 * I_sh * H * bf + R * H * bf
+                       + (T * H * bf if n_sh else 0) + R * I * bf + T * n_sh * I_sh * bf,
+                       flops=2 * 2 * H * I * R + 2 * 2 * H * n_sh * I_sh * T)
+    w["ffn_down"] = dict(bytes=active * H * I * bf + n_sh * H * I_sh * bf + R * I * bf
+                         + T * n_sh * I_sh * bf + R * H * bf + (T * H * bf if n_sh else 0),
+                         flops=2 * H * I * R + 2 * H * n_sh * I_sh * T)
+    w["combine"] = dict(bytes=R * H * bf + (T * H * bf if n_sh else 0) + T * k * 8 + T * H * bf, flops=0)
+    return w
+
+
+def source_digest() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2606_15177_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel_stage: str, workload: str):
+    """HBM bytes per launch from a committed rocprofv3 --pmc summary, if it
+    was taken on the current kernel sources (else None)."""
+    path = os.path.join(ROOT, "profiles", f"pmc_{kernel_stage}_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_src = re.search(r"source_digest:\s*([0-9a-f]+)", text)
+    m_b = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m_src or not m_b or m_src.group(1) != source_digest():
+        return None
+    return float(m_b.group(1))
+
+
+def cpu_baseline(cfg, wl, budget_s: float) -> dict:
+    """The CPU oracle (plain C, fp64, single thread) on a bounded sample of
+    the same workload: the first n tokens, n sized to the time budget."""
+    from oracle import oracle
+    oracle.lib()
+    t0 = time.perf_counter()
+    oracle.forward_tokens(cfg.dims, [0], wl["logits"], wl["x"], wl["local_experts"], wl)
+    per_tok = max(time.perf_counter() - t0, 1e-6)
+    n = int(max(1, min(cfg.T, budget_s / per_tok)))
+    toks = list(range(n))
+    t0 = time.perf_counter()
+    oracle.forward_tokens(cfg.dims, toks, wl["logits"], wl["x"], wl["local_experts"], wl)
+    dt = time.perf_counter() - t0
+    return {"value": n / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {n} of {cfg.T} tokens of {cfg.name}: per-token routing + "
+                      f"SwiGLU experts + combine, fp64, single thread ({dt:.1f} s)"}
+
+
+def main(argv=None) -> int:
+    args = parse_args(argv)
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU's MoE layer; --gpus {args.gpus} is not supported "
+              "(this build runs on a single GPU)", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2606_15177_amd import moe
+    from paper_2606_15177_amd import workloads as W
+
+    cfg = W.CONFIGS[args.config]
+    torch.cuda.set_device(0)
+    print(f"[bench] generating {cfg.name} (seed {args.seed})", file=sys.stderr, flush=True)
+    wl = W.make_workload(cfg, args.seed)
+
+    def dev(a):
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).cuda().view(torch.bfloat16)
+        return torch.from_numpy(a).cuda()
+
+    d = moe.dims_of(cfg)
+    weights = {k: dev(wl[k]) for k in ("w_gate", "w_up", "w_down", "sh_gate", "sh_up", "sh_down")
+               if k in wl}
+    local = None if wl["local_experts"] is None else dev(wl["local_experts"])
+    layer = moe.MoeLayer(d, weights, local)
+    logits, src, x = dev(wl["logits"]), dev(wl["src"]), dev(wl["x"])
+    counts = torch.zeros((cfg.S, cfg.E), dtype=torch.int64, device="cuda")
+    out = torch.empty((cfg.T, cfg.H), dtype=torch.bfloat16, device="cuda")
+    offsets = torch.empty((cfg.E_local + 1,), dtype=torch.int32, device="cuda")
+
+    n_ev = 2 * len(STAGES)
+    events = HipEvents(n_ev * args.steps)
+    step_taps = [moe.make_taps(offsets=offsets, events=events.ev[i * n_ev:(i + 1) * n_ev])
+                 for i in range(args.steps)]
+    plain_taps = moe.make_taps(offsets=offsets)
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        layer.forward(logits, src, x, counts, out, plain_taps)
+    torch.cuda.synchronize()
+
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        layer.forward(logits, src, x, counts, out, step_taps[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+
+    stage_ms = {}
+    for s, name in enumerate(STAGES):
+        vals = [events.elapsed_ms(i * n_ev + 2 * s, i * n_ev + 2 * s + 1) for i in range(args.steps)]
+        stage_ms[name] = sum(vals) / len(vals)
+    events.close()
+
+    off = offsets.cpu().numpy()
+    R = int(off[-1])
+    active = int((np.diff(off) > 0).sum())
+    work = stage_work(cfg, R, active)
+    ridge = MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+    stages = {}
+    for name in STAGES:
+        t = stage_ms[name] * 1e-3
+        b, f = work[name]["bytes"], work[name]["flops"]
+        gbs = b / t / 1e9 if t > 0 else 0.0
+        tfl = f / t / 1e12 if t > 0 else 0.0
+        stages[name] = {"ms": round(stage_ms[name], 4), "bytes": b, "flops": f,
+                        "GB/s": round(gbs, 1), "frac_hbm": round(gbs / HBM_PEAK_GBS, 4),
+                        "TFLOP/s": round(tfl, 1), "frac_mfma": round(tfl / MFMA_BF16_PEAK_TFLOPS, 4),
+                        "bound": "mfma" if f > ridge * b else "hbm"}
+    dom = max(STAGES, key=lambda n: stage_ms[n])
+    ds = stages[dom]
+    if ds["bound"] == "mfma":
+        roof = {"bound": "mfma", "achieved": ds["TFLOP/s"], "peak": MFMA_BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": ds["frac_mfma"]}
+    else:
+        roof = {"bound": "hbm", "achieved": ds["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": ds["frac_hbm"]}
+    roof["traffic"] = measured_traffic(dom, cfg.name)
+    roof["kernel"] = dom
+    ffn_ms = stage_ms["ffn_up"] + stage_ms["ffn_down"]
+    ffn_flops = work["ffn_up"]["flops"] + work["ffn_down"]["flops"]
+    ffn_frac_mfma = ffn_flops / (ffn_ms * 1e-3) / (MFMA_BF16_PEAK_TFLOPS * 1e12) if ffn_ms > 0 else 0.0
+    ffn_bytes = work["ffn_up"]["bytes"] + work["ffn_down"]["bytes"]
+    ffn_frac_hbm = ffn_bytes / (ffn_ms * 1e-3) / (HBM_PEAK_GBS * 1e9) if ffn_ms > 0 else 0.0
+
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib * (1 << 20)
+        a = torch.empty(n, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+
+    result = {
+        "metric": METRIC,
+        "value": round(cfg.T / (ms_per_step * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "T": cfg.T, "H": cfg.H, "E": cfg.E, "k": cfg.k, "I": cfg.I,
+                   "S": cfg.S, "E_local": cfg.E_local, "n_shared": cfg.n_shared,
+                   "I_shared": cfg.I_shared if cfg.n_shared else 0, "parallelism": "single GPU"},
+        "roofline": roof,
+        "expert_ffn": {"ms": round(ffn_ms, 4), "frac_mfma": round(ffn_frac_mfma, 4),
+                       "frac_hbm": round(ffn_frac_hbm, 4)},
+        "route_permute_frac_hbm": {"route": stages["route"]["frac_hbm"],
+                                   "permute": stages["permute"]["frac_hbm"],
+                                   "combine": stages["combine"]["frac_hbm"]},
+        "stages": stages,
+        "rows_local": R,
+        "active_experts": active,
+        "device": torch.cuda.get_device_name(0),
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] CPU oracle baseline", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(cfg, wl, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,256 @@
+/*
+ * moe.h -- C ABI of the MI355X (gfx950) MoE-layer hot path.
+ *
+ * One GPU's Mixture-of-Experts layer, the data-parallel path that source-aware
+ * expert placement acts on: every token is tagged with the DP engine it
+ * entered through, routed to its top-k experts, counted into the
+ * source x expert matrix, dispatched to the experts hosted on this GPU, run
+ * through their SwiGLU feed-forward networks and combined back into token
+ * order.
+ *
+ * Conventions shared by every entry point
+ *  - All array arguments are DEVICE pointers; moe_dims, moe_weights and
+ *    moe_taps structs are HOST pointers read during the call only.
+ *  - The caller owns every buffer.  The library never allocates, frees or
+ *    synchronises and keeps no mutable global state; each call only enqueues
+ *    kernels on `stream` (a hipStream_t passed as void*, NULL = the default
+ *    stream) and returns.  Results are ready when the stream reaches them.
+ *  - Every check below is made on the host before anything is enqueued; a
+ *    call that returns an error has enqueued nothing.  MOE_ERR_DEVICE means a
+ *    launch failed after earlier launches of the same call may have been
+ *    enqueued.
+ *  - Data-dependent sizes (rows routed to each local expert) never leave the
+ *    device: buffers indexed by routed rows are sized for the capacity T*k.
+ *  - bf16 values are raw IEEE bf16 bit patterns (moe_bf16).  Every bf16 and
+ *    fp32 array must be 16-byte aligned with rows whose byte length is a
+ *    multiple of 16 (H and I multiples of 8), or the call returns
+ *    MOE_ERR_ALIGN / MOE_ERR_UNSUPPORTED.
+ *  - Calls are re-entrant.  Calls that overlap on different streams may share
+ *    read-only inputs and the `counts` matrix (integer atomics); they must not
+ *    share outputs or workspace.
+ */
+#ifndef MOE_H
+#define MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MOE_ABI_VERSION 1
+
+typedef uint16_t moe_bf16;
+
+/* Status codes returned by every entry point. */
+enum moe_status {
+    MOE_OK = 0,
+    MOE_ERR_NULL = -1,        /* a required pointer is NULL */
+    MOE_ERR_DIMS = -2,        /* inconsistent or negative dimensions */
+    MOE_ERR_UNSUPPORTED = -3, /* valid, but beyond the kernels' limits */
+    MOE_ERR_WORKSPACE = -4,   /* workspace missing or smaller than required */
+    MOE_ERR_DEVICE = -5,      /* a kernel launch failed (e.g. not a gfx950 device) */
+    MOE_ERR_ALIGN = -6        /* a pointer is not 16-byte aligned */
+};
+
+/*
+ * Problem sizes (the paper's notation where it has one).
+ *   T         tokens in the batch; each carries a source DP engine id (Sec. 1,
+ *             Sec. 5.1: the "source" of the MoE traffic).
+ *   H         hidden size.
+ *   E         routed experts the router chooses among (gating width).
+ *   k         experts selected per token (top-k, Sec. 2.1), 1 <= k <= E.
+ *   I         intermediate size of a routed expert's SwiGLU FFN.
+ *   S         number of source DP engines; source ids lie in [0, S).
+ *   E_local   experts hosted on this GPU (its slice of the placement
+ *             x_{l,e,g}, Sec. 5.2), 1 <= E_local <= E.
+ *   n_shared  always-on shared experts applied to every token (0 = none).
+ *   I_shared  intermediate size of each shared expert (ignored if n_shared=0).
+ *   flags     must be 0 (reserved for gating variants).
+ * Kernel limits (MOE_ERR_UNSUPPORTED beyond them): E <= 1024, k <= 32,
+ * H, I, I_shared multiples of 8, I_shared a multiple of 64 when n_shared > 1,
+ * T*k < 2^31.
+ */
+typedef struct moe_dims {
+    int32_t T, H, E, k, I, S, E_local, n_shared, I_shared, flags;
+} moe_dims;
+
+/*
+ * Expert weights in nn.Linear layout (output features x input features),
+ * bf16, row-major, stacked by LOCAL SLOT (slot s holds global expert
+ * local_experts[s]):
+ *   w_gate, w_up  [E_local][I][H]       w_down  [E_local][H][I]
+ *   sh_gate, sh_up [n_shared][I_shared][H]   sh_down [n_shared][H][I_shared]
+ * The shared pointers may be NULL when n_shared == 0.
+ */
+typedef struct moe_weights {
+    const moe_bf16 *w_gate, *w_up, *w_down;
+    const moe_bf16 *sh_gate, *sh_up, *sh_down;
+} moe_weights;
+
+/* Which entry point a workspace size refers to. */
+enum moe_entry { MOE_ENTRY_PERMUTE = 1, MOE_ENTRY_EXPERT_FFN = 2, MOE_ENTRY_FORWARD = 3 };
+
+/* Stages of moe_forward, for the optional timing events of moe_taps. */
+enum moe_stage {
+    MOE_STAGE_ROUTE = 0,    /* top-k gating + source x expert counts */
+    MOE_STAGE_PERMUTE = 1,  /* slot counts, offsets, stable dispatch order, row gather */
+    MOE_STAGE_FFN_UP = 2,   /* gate/up GEMM with the SwiGLU epilogue (routed, then shared) */
+    MOE_STAGE_FFN_DOWN = 3, /* down GEMM (routed, then shared) */
+    MOE_STAGE_COMBINE = 4,  /* weighted combine back to token order */
+    MOE_NUM_STAGES = 5
+};
+
+/*
+ * Optional extra outputs of moe_forward; every field may be NULL.
+ *   topk_idx [T][k], topk_w [T][k], offsets [E_local+1], perm_token [T*k]
+ *   (first offsets[E_local] entries valid), inv_pos [T*k]: copies of the
+ *   intermediate results with the meaning given at the entry points below.
+ *   expert_load [E]: set (=) to this call's per-expert load B.
+ *   events[2*s], events[2*s+1]: hipEvent_t handles recorded on `stream`
+ *   immediately before the first and after the last kernel of stage s.
+ */
+typedef struct moe_taps {
+    int32_t *topk_idx;
+    float *topk_w;
+    int32_t *expert_load;
+    int32_t *offsets;
+    int32_t *perm_token;
+    int32_t *inv_pos;
+    void *events[2 * MOE_NUM_STAGES];
+} moe_taps;
+
+/* MOE_ABI_VERSION of the built library. */
+int moe_abi_version(void);
+
+/* Static text for a status code (never NULL). */
+const char *moe_strerror(int status);
+
+/*
+ * Bytes of workspace `entry` needs for these sizes (0 when the dimensions are
+ * invalid; moe_validate says why).  Host only, no HIP call.  The workspace is
+ * device memory owned by the caller, at least 256-byte aligned; its contents
+ * need no initialisation and are undefined after the call.
+ */
+size_t moe_workspace_bytes(const moe_dims *dims, int entry);
+
+/*
+ * Host-only check of dims (and, when entry != 0, of ws_bytes against
+ * moe_workspace_bytes(dims, entry)).  Returns MOE_OK or the status the entry
+ * points would return for these sizes.  Makes no HIP call.
+ */
+int moe_validate(const moe_dims *dims, int entry, size_t ws_bytes);
+
+/*
+ * Top-k gating (Sec. 2.1: the router selects the top-k experts of each token).
+ *   logits    [T][E] fp32, row-major, any bias already added.
+ *   topk_idx  [T][k] int32 out: the k selected experts of each token, ordered
+ *             by logit descending; equal logits (-0.0 equals +0.0) go to the
+ *             lower expert index; NaN ranks below every number.
+ *   topk_w    [T][k] fp32 out: gates, the softmax of the selected logits
+ *             renormalised over the k selected (NaN when the largest selected
+ *             logit is not finite).
+ * Uses T, E, k.  T = 0 is a no-op.
+ */
+int moe_route(const moe_dims *dims, const float *logits, int32_t *topk_idx,
+              float *topk_w, void *stream);
+
+/*
+ * Source-aware routing statistics (Sec. 5.1: the source x expert matrix
+ * A_{l,s,e} and the aggregate load B_{l,e}).
+ *   src          [T] int32: source DP engine of each token, expected in [0, S).
+ *   topk_idx     [T][k] int32: expert ids, expected in [0, E).
+ *   counts       [S][E] int64, ACCUMULATED (+=): one per pair (t, j) with
+ *                src[t] = s and topk_idx[t][j] = e.  The caller keeps one
+ *                buffer per layer and zeroes it to start a profiling window.
+ *   expert_load  [E] int32, nullable, SET (=) to this call's column sums of
+ *                the added counts.
+ * A pair whose source or expert id is out of range is not counted (the call
+ * stays in bounds; it does not report the bad id).  Uses T, E, k, S.
+ */
+int moe_route_stats(const moe_dims *dims, const int32_t *src,
+                    const int32_t *topk_idx, int64_t *counts,
+                    int32_t *expert_load, void *stream);
+
+/*
+ * Dispatch to the local experts (Sec. 2.1 dispatch; Sec. 5.2 placement slice).
+ *   local_experts [E_local] int32, nullable: global expert hosted in each local
+ *                 slot, distinct and in [0, E).  NULL means slot = expert id
+ *                 and requires E_local == E.
+ *   offsets       [E_local+1] int32 out: slot s owns rows
+ *                 [offsets[s], offsets[s+1]); offsets[E_local] = R, the number
+ *                 of pairs routed to local experts.
+ *   perm_token    [T*k] int32 out: row r < R holds token perm_token[r]; rows
+ *                 follow slot order, tokens ascending within a slot.
+ *   inv_pos       [T*k] int32 out: row of pair (t, j) at t*k+j, or -1 when its
+ *                 expert is not hosted here.
+ *   x             [T][H] bf16 and x_perm [T*k][H] bf16 out: x_perm[r] =
+ *                 x[perm_token[r]]; both may be NULL to skip the row gather.
+ *   ws            MOE_ENTRY_PERMUTE workspace.
+ * Expert ids outside [0, E) are treated as remote.  T = 0 sets offsets to 0.
+ */
+int moe_permute(const moe_dims *dims, const int32_t *topk_idx,
+                const int32_t *local_experts, const moe_bf16 *x,
+                int32_t *offsets, int32_t *perm_token, int32_t *inv_pos,
+                moe_bf16 *x_perm, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * The experts' SwiGLU feed-forward networks as grouped GEMMs (Sec. 2.1: each
+ * token activates only its experts' feed-forward parameters):
+ *   y_perm[r] = W_down[s] (silu(W_gate[s] x_perm[r]) * (W_up[s] x_perm[r]))
+ * for every row r in [offsets[s], offsets[s+1]), silu(z) = z / (1 + e^-z),
+ * with fp32 accumulation and the intermediate rounded to bf16, and
+ *   y_shared[t] = sum_q FFN^shared_q(x[t])   (fp32 sum, then bf16)
+ * when n_shared > 0.
+ *   x_perm   [T*k][H] bf16, rows [0, offsets[E_local]) read.
+ *   offsets  [E_local+1] int32 as written by moe_permute.
+ *   weights  see moe_weights.
+ *   x        [T][H] bf16 (read only when n_shared > 0).
+ *   y_perm   [T*k][H] bf16 out, rows [0, offsets[E_local]) written.
+ *   y_shared [T][H] bf16 out (required when n_shared > 0, else ignored).
+ *   ws       MOE_ENTRY_EXPERT_FFN workspace.
+ */
+int moe_expert_ffn(const moe_dims *dims, const moe_bf16 *x_perm,
+                   const int32_t *offsets, const moe_weights *weights,
+                   const moe_bf16 *x, moe_bf16 *y_perm, moe_bf16 *y_shared,
+                   void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Weighted combine back to token order (Sec. 2.1: expert outputs are
+ * combined and returned):
+ *   out[t] = sum_{j<k, inv_pos[t*k+j] >= 0} topk_w[t][j] * y_perm[inv_pos[t*k+j]]
+ *            + y_shared[t]
+ * accumulated in fp32 in j order, then rounded to bf16.  Tokens none of whose
+ * experts are local get y_shared[t] (or zeros).
+ *   y_perm [T*k][H] bf16; inv_pos [T*k] int32 (entries must be -1 or a row
+ *   written by moe_expert_ffn); topk_w [T][k] fp32; y_shared [T][H] bf16,
+ *   nullable; out [T][H] bf16 out.
+ */
+int moe_combine(const moe_dims *dims, const moe_bf16 *y_perm,
+                const int32_t *inv_pos, const float *topk_w,
+                const moe_bf16 *y_shared, moe_bf16 *out, void *stream);
+
+/*
+ * The whole layer: moe_route (+ moe_route_stats) -> moe_permute ->
+ * moe_expert_ffn -> moe_combine, with the intermediates in the workspace.
+ *   logits [T][E] fp32; src [T] int32 (nullable when counts is NULL);
+ *   x [T][H] bf16; local_experts as in moe_permute; weights as in
+ *   moe_expert_ffn;
+ *   counts [S][E] int64, nullable: accumulated as in moe_route_stats (NULL
+ *          skips the statistics);
+ *   out [T][H] bf16 out: the layer output for this GPU's experts
+ *          (plus the shared experts);
+ *   taps   nullable host struct of optional extra outputs and events;
+ *   ws     MOE_ENTRY_FORWARD workspace.
+ */
+int moe_forward(const moe_dims *dims, const float *logits, const int32_t *src,
+                const moe_bf16 *x, const int32_t *local_experts,
+                const moe_weights *weights, int64_t *counts, moe_bf16 *out,
+                const moe_taps *taps, void *ws, size_t ws_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOE_H */

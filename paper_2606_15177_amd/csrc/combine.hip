@@ -1,0 +1,80 @@
+// Weighted combine back to token order (Sec. 2.1: expert outputs are
+// combined and returned):
+//   out[t] = sum_{j<k, inv_pos[t*k+j] >= 0} w[t][j] * y_perm[inv_pos[t*k+j]] + y_shared[t]
+// One wave per token; each lane owns 16-byte column vectors of the row and
+// accumulates in fp32, j ascending then the shared term, so the result does
+// not depend on scheduling.  Bandwidth-bound: every byte is read once.
+#include "common.h"
+#include "kernels.h"
+
+namespace moe {
+namespace {
+
+constexpr int kMaxK = 32;
+
+__global__ __launch_bounds__(256) void combine_kernel(int T, int k, int H,
+                                                      const uint16_t* __restrict__ y_perm,
+                                                      const int32_t* __restrict__ inv_pos,
+                                                      const float* __restrict__ topk_w,
+                                                      const uint16_t* __restrict__ y_shared,
+                                                      uint16_t* __restrict__ out) {
+  const int lane = lane_id();
+  const int n_waves = gridDim.x * (blockDim.x / kWave);
+  const int vpr = H / 8;
+  for (int t = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave; t < T; t += n_waves) {
+    // the token's k (row, weight) pairs, gathered once per wave
+    int pos = -1;
+    float w = 0.0f;
+    if (lane < k) {
+      pos = inv_pos[static_cast<size_t>(t) * k + lane];
+      w = topk_w[static_cast<size_t>(t) * k + lane];
+    }
+    // the whole wave walks the row in lock-step so every lane takes part in
+    // the shuffles; lanes past the end of the row only skip the memory work
+    for (int v0 = 0; v0 < vpr; v0 += kWave) {
+      const int v = v0 + lane;
+      const bool active = v < vpr;
+      float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < k; ++j) {
+        const int r = __shfl(pos, j);
+        const float wj = __shfl(w, j);
+        if (r < 0 || !active) continue;
+        const u32x4 q = load16(y_perm + static_cast<size_t>(r) * H + v * 8);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc[2 * e] = fmaf(wj, __uint_as_float(q[e] << 16), acc[2 * e]);
+          acc[2 * e + 1] = fmaf(wj, __uint_as_float(q[e] & 0xffff0000u), acc[2 * e + 1]);
+        }
+      }
+      if (!active) continue;
+      if (y_shared) {
+        const u32x4 q = load16(y_shared + static_cast<size_t>(t) * H + v * 8);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc[2 * e] += __uint_as_float(q[e] << 16);
+          acc[2 * e + 1] += __uint_as_float(q[e] & 0xffff0000u);
+        }
+      }
+      u32x4 o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = pack_bf16x2(acc[2 * e], acc[2 * e + 1]);
+      store16(out + static_cast<size_t>(t) * H + v * 8, o);
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_combine(int T, int k, int H, const uint16_t* y_perm, const int32_t* inv_pos,
+                          const float* topk_w, const uint16_t* y_shared, uint16_t* out,
+                          hipStream_t st) {
+  if (T == 0) return hipSuccess;
+  if (k > kMaxK) return hipErrorInvalidValue;
+  const int waves_per_block = 4;
+  const int blocks = min(ceil_div(T, waves_per_block), 8192);
+  hipLaunchKernelGGL(combine_kernel, dim3(blocks), dim3(waves_per_block * kWave), 0, st, T, k, H,
+                     y_perm, inv_pos, topk_w, y_shared, out);
+  return hipGetLastError();
+}
+
+}  // namespace moe

@@ -1,0 +1,77 @@
+// Host-side launchers of the gfx950 kernels; the C ABI composes them.
+// Every launcher only enqueues work on `st` and returns hipGetLastError().
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace moe {
+
+// ---- route.hip -------------------------------------------------------------
+// Top-k selection + gates; when counts != nullptr also accumulates the
+// source x expert counts (and sets expert_load if non-null, which must have
+// been zeroed on the stream before).
+hipError_t launch_route(int T, int E, int k, const float* logits, int32_t* topk_idx,
+                        float* topk_w, const int32_t* src, int S, int64_t* counts,
+                        int32_t* expert_load, hipStream_t st);
+// Counts from (src, topk_idx); expert_load as above.
+hipError_t launch_route_stats(int T, int k, int S, int E, const int32_t* src,
+                              const int32_t* topk_idx, int64_t* counts, int32_t* expert_load,
+                              hipStream_t st);
+hipError_t launch_fill_i32(int32_t* p, int n, int32_t value, hipStream_t st);
+
+// ---- permute.hip -----------------------------------------------------------
+size_t permute_ws_bytes(int T, int k, int E_local);
+// offsets / perm_token / inv_pos of the stable dispatch sort.
+hipError_t launch_permute(int T, int k, int E, int E_local, const int32_t* local_experts,
+                          const int32_t* topk_idx, int32_t* offsets, int32_t* perm_token,
+                          int32_t* inv_pos, void* ws, hipStream_t st);
+// x_perm[r] = x[perm_token[r]] for r < *n_rows (device scalar), capacity rows.
+hipError_t launch_gather_rows(int capacity, int H, const int32_t* perm_token,
+                              const int32_t* n_rows, const uint16_t* x, uint16_t* x_perm,
+                              hipStream_t st);
+
+// ---- ffn_*.hip -------------------------------------------------------------
+// A grouped GEMM over row segments.  Group g owns rows [offsets[g],
+// offsets[g+1]) of the activation matrix (or rows [0, static_rows) of a single
+// group when offsets == nullptr).  max_rows bounds the rows of any one group
+// and total_rows the rows of all groups (both host-side capacities).
+struct Segments {
+  const int32_t* offsets;
+  int groups;
+  int static_rows;
+  int max_rows;
+  int total_rows;
+};
+
+// h[r][i] = silu(sum_c x[r][c] Wg[g][i][c]) * (sum_c x[r][c] Wu[g][i][c]),
+// weights [groups][N][K] (group stride N*K), x row stride K, h row stride N.
+struct UpArgs {
+  const uint16_t* x;
+  const uint16_t* w_gate;
+  const uint16_t* w_up;
+  uint16_t* h;
+  int K, N;
+};
+hipError_t launch_ffn_up(const Segments& seg, const UpArgs& a, hipStream_t st);
+
+// y[r][n] = sum_c h[r][c] Wd(g, n, c), h row stride K, y row stride N.
+// Wd(g, n, c) = w[g*group_stride + (c / kseg)*seg_stride + n*ldw + c % kseg]
+// (one segment per group for routed experts; the stacked shared experts use
+// kseg = I_shared so that the K range runs over all of them).
+struct DownArgs {
+  const uint16_t* h;
+  const uint16_t* w;
+  uint16_t* y;
+  int K, N, kseg, ldw;
+  size_t seg_stride, group_stride;
+};
+hipError_t launch_ffn_down(const Segments& seg, const DownArgs& a, hipStream_t st);
+
+// ---- combine.hip -----------------------------------------------------------
+hipError_t launch_combine(int T, int k, int H, const uint16_t* y_perm, const int32_t* inv_pos,
+                          const float* topk_w, const uint16_t* y_shared, uint16_t* out,
+                          hipStream_t st);
+
+}  // namespace moe

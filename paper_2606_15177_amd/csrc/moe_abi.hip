@@ -1,0 +1,324 @@
+// The C ABI (include/moe.h): host-side validation, workspace carving and the
+// launch sequence of each entry point.  No allocation, no synchronisation,
+// no device-to-host traffic: every data-dependent size stays on the device.
+#include "moe.h"
+
+#include <algorithm>
+
+#include "kernels.h"
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int64_t kIntMax = 2147483647;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_dims(const moe_dims* d) {
+  if (d == nullptr) return MOE_ERR_NULL;
+  if (d->T < 0 || d->H < 1 || d->E < 1 || d->k < 1 || d->k > d->E || d->I < 1 || d->S < 1 ||
+      d->E_local < 1 || d->E_local > d->E || d->n_shared < 0 ||
+      (d->n_shared > 0 && d->I_shared < 1))
+    return MOE_ERR_DIMS;
+  if (d->flags != 0) return MOE_ERR_UNSUPPORTED;
+  if (d->E > 1024 || d->k > 32) return MOE_ERR_UNSUPPORTED;
+  if (d->H % 8 != 0 || d->I % 8 != 0 || (d->n_shared > 0 && d->I_shared % 8 != 0))
+    return MOE_ERR_UNSUPPORTED;
+  if (static_cast<int64_t>(d->T) * d->k > kIntMax || static_cast<int64_t>(d->S) * d->E > kIntMax ||
+      static_cast<int64_t>(d->n_shared) * std::max(d->I_shared, 0) > kIntMax)
+    return MOE_ERR_UNSUPPORTED;
+  return MOE_OK;
+}
+
+int64_t sh_width(const moe_dims* d) {
+  return d->n_shared > 0 ? static_cast<int64_t>(d->n_shared) * d->I_shared : 0;
+}
+
+size_t ffn_ws(const moe_dims* d) {
+  const size_t rows = static_cast<size_t>(d->T) * d->k;
+  size_t b = align_up(rows * d->I * sizeof(uint16_t));                           // h
+  b += align_up(static_cast<size_t>(d->T) * sh_width(d) * sizeof(uint16_t));   // h_shared
+  return b;
+}
+
+// The forward workspace, carved in this order.
+struct ForwardWs {
+  int32_t* topk_idx;
+  float* topk_w;
+  int32_t* offsets;
+  int32_t* perm_token;
+  int32_t* inv_pos;
+  uint16_t* x_perm;
+  uint16_t* y_perm;
+  uint16_t* y_shared;
+  void* permute_ws;
+  void* ffn_ws;
+  size_t bytes;
+};
+
+ForwardWs carve_forward(const moe_dims* d, void* base) {
+  ForwardWs w{};
+  unsigned char* p = static_cast<unsigned char*>(base);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    unsigned char* r = p ? p + off : nullptr;
+    off += align_up(bytes);
+    return r;
+  };
+  const size_t rows = static_cast<size_t>(d->T) * d->k;
+  w.topk_idx = reinterpret_cast<int32_t*>(take(rows * sizeof(int32_t)));
+  w.topk_w = reinterpret_cast<float*>(take(rows * sizeof(float)));
+  w.offsets = reinterpret_cast<int32_t*>(take((d->E_local + 1) * sizeof(int32_t)));
+  w.perm_token = reinterpret_cast<int32_t*>(take(rows * sizeof(int32_t)));
+  w.inv_pos = reinterpret_cast<int32_t*>(take(rows * sizeof(int32_t)));
+  w.x_perm = reinterpret_cast<uint16_t*>(take(rows * d->H * sizeof(uint16_t)));
+  w.y_perm = reinterpret_cast<uint16_t*>(take(rows * d->H * sizeof(uint16_t)));
+  w.y_shared = reinterpret_cast<uint16_t*>(
+      take(d->n_shared > 0 ? static_cast<size_t>(d->T) * d->H * sizeof(uint16_t) : 0));
+  w.permute_ws = take(moe::permute_ws_bytes(d->T, d->k, d->E_local));
+  w.ffn_ws = take(ffn_ws(d));
+  w.bytes = off;
+  return w;
+}
+
+size_t entry_ws(const moe_dims* d, int entry) {
+  switch (entry) {
+    case MOE_ENTRY_PERMUTE:
+      return align_up(moe::permute_ws_bytes(d->T, d->k, d->E_local));
+    case MOE_ENTRY_EXPERT_FFN:
+      return ffn_ws(d);
+    case MOE_ENTRY_FORWARD:
+      return carve_forward(d, nullptr).bytes;
+    default:
+      return 0;
+  }
+}
+
+int check_ws(const moe_dims* d, int entry, const void* ws, size_t ws_bytes) {
+  const size_t need = entry_ws(d, entry);
+  if (ws_bytes < need) return MOE_ERR_WORKSPACE;
+  if (need > 0 && ws == nullptr) return MOE_ERR_WORKSPACE;
+  if (ws != nullptr && (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0) return MOE_ERR_ALIGN;
+  return MOE_OK;
+}
+
+int status(hipError_t e) { return e == hipSuccess ? MOE_OK : MOE_ERR_DEVICE; }
+
+void record(const moe_taps* taps, int slot, hipStream_t st) {
+  if (taps && taps->events[slot]) (void)hipEventRecord(static_cast<hipEvent_t>(taps->events[slot]), st);
+}
+
+int weights_ok(const moe_dims* d, const moe_weights* w) {
+  if (w == nullptr || w->w_gate == nullptr || w->w_up == nullptr || w->w_down == nullptr)
+    return MOE_ERR_NULL;
+  if (d->n_shared > 0 && (w->sh_gate == nullptr || w->sh_up == nullptr || w->sh_down == nullptr))
+    return MOE_ERR_NULL;
+  if (!aligned16(w->w_gate) || !aligned16(w->w_up) || !aligned16(w->w_down)) return MOE_ERR_ALIGN;
+  if (d->n_shared > 0 && (!aligned16(w->sh_gate) || !aligned16(w->sh_up) || !aligned16(w->sh_down)))
+    return MOE_ERR_ALIGN;
+  return MOE_OK;
+}
+
+// The two grouped GEMMs of the experts (routed, then shared) + their events.
+int run_ffn(const moe_dims* d, const uint16_t* x_perm, const int32_t* offsets,
+            const moe_weights* w, const uint16_t* x, uint16_t* y_perm, uint16_t* y_shared,
+            void* ws, const moe_taps* taps, hipStream_t st) {
+  const size_t rows = static_cast<size_t>(d->T) * d->k;
+  uint16_t* h = static_cast<uint16_t*>(ws);
+  uint16_t* h_sh = reinterpret_cast<uint16_t*>(static_cast<unsigned char*>(ws) +
+                                               align_up(rows * d->I * sizeof(uint16_t)));
+  const int shw = static_cast<int>(sh_width(d));
+  const moe::Segments routed{offsets, d->E_local, 0, d->T, d->T * d->k};
+  const moe::Segments shared{nullptr, 1, d->T, d->T, d->T};
+  hipError_t e;
+
+  record(taps, 2 * MOE_STAGE_FFN_UP, st);
+  e = moe::launch_ffn_up(routed, moe::UpArgs{x_perm, w->w_gate, w->w_up, h, d->H, d->I}, st);
+  if (e != hipSuccess) return MOE_ERR_DEVICE;
+  if (d->n_shared > 0) {
+    e = moe::launch_ffn_up(shared, moe::UpArgs{x, w->sh_gate, w->sh_up, h_sh, d->H, shw}, st);
+    if (e != hipSuccess) return MOE_ERR_DEVICE;
+  }
+  record(taps, 2 * MOE_STAGE_FFN_UP + 1, st);
+
+  record(taps, 2 * MOE_STAGE_FFN_DOWN, st);
+  moe::DownArgs dn{h, w->w_down, y_perm, d->I, d->H, d->I, d->I, 0,
+                   static_cast<size_t>(d->H) * d->I};
+  e = moe::launch_ffn_down(routed, dn, st);
+  if (e != hipSuccess) return MOE_ERR_DEVICE;
+  if (d->n_shared > 0) {
+    moe::DownArgs ds{h_sh, w->sh_down, y_shared, shw, d->H, d->I_shared, d->I_shared,
+                     static_cast<size_t>(d->H) * d->I_shared, 0};
+    e = moe::launch_ffn_down(shared, ds, st);
+    if (e != hipSuccess) return MOE_ERR_DEVICE;
+  }
+  record(taps, 2 * MOE_STAGE_FFN_DOWN + 1, st);
+  return MOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int moe_abi_version(void) { return MOE_ABI_VERSION; }
+
+const char* moe_strerror(int s) {
+  switch (s) {
+    case MOE_OK: return "ok";
+    case MOE_ERR_NULL: return "a required pointer is NULL";
+    case MOE_ERR_DIMS: return "inconsistent or negative dimensions";
+    case MOE_ERR_UNSUPPORTED: return "dimensions beyond the kernels' limits";
+    case MOE_ERR_WORKSPACE: return "workspace missing or too small";
+    case MOE_ERR_DEVICE: return "kernel launch failed";
+    case MOE_ERR_ALIGN: return "pointer not 16-byte aligned";
+    default: return "unknown status";
+  }
+}
+
+size_t moe_workspace_bytes(const moe_dims* d, int entry) {
+  if (check_dims(d) != MOE_OK) return 0;
+  return entry_ws(d, entry);
+}
+
+int moe_validate(const moe_dims* d, int entry, size_t ws_bytes) {
+  int s = check_dims(d);
+  if (s != MOE_OK) return s;
+  if (entry != 0 && ws_bytes < entry_ws(d, entry)) return MOE_ERR_WORKSPACE;
+  return MOE_OK;
+}
+
+int moe_route(const moe_dims* d, const float* logits, int32_t* topk_idx, float* topk_w,
+              void* stream) {
+  int s = check_dims(d);
+  if (s != MOE_OK) return s;
+  if (d->T > 0 && (!logits || !topk_idx || !topk_w)) return MOE_ERR_NULL;
+  return status(moe::launch_route(d->T, d->E, d->k, logits, topk_idx, topk_w, nullptr, d->S,
+                                  nullptr, nullptr, static_cast<hipStream_t>(stream)));
+}
+
+int moe_route_stats(const moe_dims* d, const int32_t* src, const int32_t* topk_idx,
+                    int64_t* counts, int32_t* expert_load, void* stream) {
+  int s = check_dims(d);
+  if (s != MOE_OK) return s;
+  if (!counts || (d->T > 0 && (!src || !topk_idx))) return MOE_ERR_NULL;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (expert_load && moe::launch_fill_i32(expert_load, d->E, 0, st) != hipSuccess)
+    return MOE_ERR_DEVICE;
+  return status(moe::launch_route_stats(d->T, d->k, d->S, d->E, src, topk_idx, counts,
+                                        expert_load, st));
+}
+
+int moe_permute(const moe_dims* d, const int32_t* topk_idx, const int32_t* local_experts,
+                const moe_bf16* x, int32_t* offsets, int32_t* perm_token, int32_t* inv_pos,
+                moe_bf16* x_perm, void* ws, size_t ws_bytes, void* stream) {
+  int s = check_dims(d);
+  if (s != MOE_OK) return s;
+  if (!local_experts && d->E_local != d->E) return MOE_ERR_DIMS;
+  if (!offsets || (d->T > 0 && (!topk_idx || !perm_token || !inv_pos))) return MOE_ERR_NULL;
+  if ((x == nullptr) != (x_perm == nullptr)) return MOE_ERR_NULL;
+  if (x && (!aligned16(x) || !aligned16(x_perm))) return MOE_ERR_ALIGN;
+  s = check_ws(d, MOE_ENTRY_PERMUTE, ws, ws_bytes);
+  if (s != MOE_OK) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = moe::launch_permute(d->T, d->k, d->E, d->E_local, local_experts, topk_idx,
+                                     offsets, perm_token, inv_pos, ws, st);
+  if (e != hipSuccess) return MOE_ERR_DEVICE;
+  if (x) {
+    e = moe::launch_gather_rows(d->T * d->k, d->H, perm_token, offsets + d->E_local, x, x_perm, st);
+    if (e != hipSuccess) return MOE_ERR_DEVICE;
+  }
+  return MOE_OK;
+}
+
+int moe_expert_ffn(const moe_dims* d, const moe_bf16* x_perm, const int32_t* offsets,
+                   const moe_weights* w, const moe_bf16* x, moe_bf16* y_perm, moe_bf16* y_shared,
+                   void* ws, size_t ws_bytes, void* stream) {
+  int s = check_dims(d);
+  if (s != MOE_OK) return s;
+  s = weights_ok(d, w);
+  if (s != MOE_OK) return s;
+  if (!x_perm || !offsets || !y_perm) return MOE_ERR_NULL;
+  if (d->n_shared > 0 && (!x || !y_shared)) return MOE_ERR_NULL;
+  if (!aligned16(x_perm) || !aligned16(y_perm)) return MOE_ERR_ALIGN;
+  if (d->n_shared > 0 && (!aligned16(x) || !aligned16(y_shared))) return MOE_ERR_ALIGN;
+  s = check_ws(d, MOE_ENTRY_EXPERT_FFN, ws, ws_bytes);
+  if (s != MOE_OK) return s;
+  if (d->T == 0) return MOE_OK;
+  return run_ffn(d, x_perm, offsets, w, x, y_perm, y_shared, ws, nullptr,
+                 static_cast<hipStream_t>(stream));
+}
+
+int moe_combine(const moe_dims* d, const moe_bf16* y_perm, const int32_t* inv_pos,
+                const float* topk_w, const moe_bf16* y_shared, moe_bf16* out, void* stream) {
+  int s = check_dims(d);
+  if (s != MOE_OK) return s;
+  if (d->T > 0 && (!y_perm || !inv_pos || !topk_w || !out)) return MOE_ERR_NULL;
+  if (d->T > 0 && (!aligned16(y_perm) || !aligned16(out) || (y_shared && !aligned16(y_shared))))
+    return MOE_ERR_ALIGN;
+  return status(moe::launch_combine(d->T, d->k, d->H, y_perm, inv_pos, topk_w, y_shared, out,
+                                    static_cast<hipStream_t>(stream)));
+}
+
+int moe_forward(const moe_dims* d, const float* logits, const int32_t* src, const moe_bf16* x,
+                const int32_t* local_experts, const moe_weights* w, int64_t* counts,
+                moe_bf16* out, const moe_taps* taps, void* ws, size_t ws_bytes, void* stream) {
+  int s = check_dims(d);
+  if (s != MOE_OK) return s;
+  if (!local_experts && d->E_local != d->E) return MOE_ERR_DIMS;
+  s = weights_ok(d, w);
+  if (s != MOE_OK) return s;
+  if (d->T > 0 && (!logits || !x || !out)) return MOE_ERR_NULL;
+  if (counts && d->T > 0 && !src) return MOE_ERR_NULL;
+  if (d->T > 0 && (!aligned16(x) || !aligned16(out))) return MOE_ERR_ALIGN;
+  s = check_ws(d, MOE_ENTRY_FORWARD, ws, ws_bytes);
+  if (s != MOE_OK) return s;
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  ForwardWs fw = carve_forward(d, ws);
+  int32_t* topk_idx = (taps && taps->topk_idx) ? taps->topk_idx : fw.topk_idx;
+  float* topk_w = (taps && taps->topk_w) ? taps->topk_w : fw.topk_w;
+  int32_t* offsets = (taps && taps->offsets) ? taps->offsets : fw.offsets;
+  int32_t* perm_token = (taps && taps->perm_token) ? taps->perm_token : fw.perm_token;
+  int32_t* inv_pos = (taps && taps->inv_pos) ? taps->inv_pos : fw.inv_pos;
+  int32_t* expert_load = taps ? taps->expert_load : nullptr;
+  hipError_t e;
+
+  record(taps, 2 * MOE_STAGE_ROUTE, st);
+  if (counts && expert_load) {
+    e = moe::launch_fill_i32(expert_load, d->E, 0, st);
+    if (e != hipSuccess) return MOE_ERR_DEVICE;
+  }
+  e = moe::launch_route(d->T, d->E, d->k, logits, topk_idx, topk_w, counts ? src : nullptr, d->S,
+                        counts, counts ? expert_load : nullptr, st);
+  if (e != hipSuccess) return MOE_ERR_DEVICE;
+  record(taps, 2 * MOE_STAGE_ROUTE + 1, st);
+
+  record(taps, 2 * MOE_STAGE_PERMUTE, st);
+  e = moe::launch_permute(d->T, d->k, d->E, d->E_local, local_experts, topk_idx, offsets,
+                          perm_token, inv_pos, fw.permute_ws, st);
+  if (e != hipSuccess) return MOE_ERR_DEVICE;
+  e = moe::launch_gather_rows(d->T * d->k, d->H, perm_token, offsets + d->E_local, x, fw.x_perm, st);
+  if (e != hipSuccess) return MOE_ERR_DEVICE;
+  record(taps, 2 * MOE_STAGE_PERMUTE + 1, st);
+
+  if (d->T > 0) {
+    s = run_ffn(d, fw.x_perm, offsets, w, x, fw.y_perm, fw.y_shared, fw.ffn_ws, taps, st);
+    if (s != MOE_OK) return s;
+  } else {
+    record(taps, 2 * MOE_STAGE_FFN_UP, st);
+    record(taps, 2 * MOE_STAGE_FFN_UP + 1, st);
+    record(taps, 2 * MOE_STAGE_FFN_DOWN, st);
+    record(taps, 2 * MOE_STAGE_FFN_DOWN + 1, st);
+  }
+
+  record(taps, 2 * MOE_STAGE_COMBINE, st);
+  e = moe::launch_combine(d->T, d->k, d->H, fw.y_perm, inv_pos, topk_w,
+                          d->n_shared > 0 ? fw.y_shared : nullptr, out, st);
+  if (e != hipSuccess) return MOE_ERR_DEVICE;
+  record(taps, 2 * MOE_STAGE_COMBINE + 1, st);
+  return MOE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,210 @@
+// Dispatch of the selected (token, expert) pairs to the locally hosted
+// experts (Sec. 2.1 dispatch; Sec. 5.2, this GPU's slice of the placement).
+//
+// A stable counting sort of the T*k pairs by local slot, in three launches
+// over tiles of kTile consecutive pairs (token-major order):
+//   1. count   per tile and slot, LDS atomics -> tile_counts[tile][slot];
+//   2. scan    one block: per-slot exclusive prefix over tiles (in place) and
+//              the exclusive prefix over slots -> offsets[0..E_local];
+//   3. scatter one wave per tile walks its pairs in order, 64 at a time; the
+//              pairs of one slot inside a 64-pair chunk are ranked with a
+//              ballot + popcount, so ties keep token order without depending
+//              on atomic order.  Writes perm_token and inv_pos.
+// The row gather x_perm[r] = x[perm_token[r]] is a fourth, bandwidth-bound
+// kernel that copies 16-byte vectors.
+#include "common.h"
+#include "kernels.h"
+
+namespace moe {
+namespace {
+
+constexpr int kTile = 512;
+
+// slot_of[e] = local slot hosting expert e, or -1.  An expert listed twice
+// (outside the documented contract) resolves to its lowest slot, the same in
+// every kernel, so the count and scatter passes always agree.  Ends with a
+// barrier.
+__device__ void build_slot_map(int* slot_of, int E, int E_local, const int32_t* local_experts) {
+  if (local_experts == nullptr) {
+    for (int e = threadIdx.x; e < E; e += blockDim.x) slot_of[e] = e;
+  } else {
+    for (int e = threadIdx.x; e < E; e += blockDim.x) slot_of[e] = E_local;
+    __syncthreads();
+    for (int s = threadIdx.x; s < E_local; s += blockDim.x) {
+      const int e = local_experts[s];
+      if (e >= 0 && e < E) atomicMin(&slot_of[e], s);
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < E; e += blockDim.x)
+      if (slot_of[e] >= E_local) slot_of[e] = -1;
+  }
+  __syncthreads();
+}
+
+__device__ __forceinline__ int slot_lookup(const int* slot_of, int e, int E) {
+  return (e >= 0 && e < E) ? slot_of[e] : -1;
+}
+
+__global__ __launch_bounds__(256) void perm_count_kernel(int n_pairs, int E, int E_local,
+                                                         const int32_t* __restrict__ local_experts,
+                                                         const int32_t* __restrict__ topk_idx,
+                                                         int32_t* __restrict__ tile_counts) {
+  extern __shared__ int sm[];
+  int* slot_of = sm;
+  int* cnt = sm + E;
+  for (int s = threadIdx.x; s < E_local; s += blockDim.x) cnt[s] = 0;
+  build_slot_map(slot_of, E, E_local, local_experts);
+  const int p0 = blockIdx.x * kTile;
+  const int p1 = min(n_pairs, p0 + kTile);
+  for (int p = p0 + threadIdx.x; p < p1; p += blockDim.x) {
+    const int s = slot_lookup(slot_of, topk_idx[p], E);
+    if (s >= 0) atomicAdd(&cnt[s], 1);
+  }
+  __syncthreads();
+  for (int s = threadIdx.x; s < E_local; s += blockDim.x)
+    tile_counts[static_cast<size_t>(blockIdx.x) * E_local + s] = cnt[s];
+}
+
+// Exclusive scan of one value per thread over a block of blockDim.x threads
+// (a multiple of 64, at most 1024).  Returns the exclusive prefix; *total
+// receives the block sum.  Ends with a barrier.
+__device__ int block_exclusive_scan(int v, int* total) {
+  __shared__ int wsum[16];
+  const int lane = lane_id();
+  const int wave = threadIdx.x / kWave;
+  int inc = v;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const int o = __shfl_up(inc, off);
+    if (lane >= off) inc += o;
+  }
+  if (lane == kWave - 1) wsum[wave] = inc;
+  __syncthreads();
+  if (wave == 0) {
+    const int n_waves = blockDim.x / kWave;
+    int w = lane < n_waves ? wsum[lane] : 0;
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) {
+      const int o = __shfl_up(w, off);
+      if (lane >= off) w += o;
+    }
+    if (lane < n_waves) wsum[lane] = w;  // inclusive over waves
+  }
+  __syncthreads();
+  const int before = wave > 0 ? wsum[wave - 1] : 0;
+  *total = wsum[blockDim.x / kWave - 1];
+  __syncthreads();
+  return before + inc - v;
+}
+
+__global__ __launch_bounds__(1024) void perm_scan_kernel(int n_tiles, int E_local,
+                                                         int32_t* __restrict__ tile_counts,
+                                                         int32_t* __restrict__ offsets) {
+  const int s = threadIdx.x;
+  int running = 0;
+  if (s < E_local) {
+    for (int tile = 0; tile < n_tiles; ++tile) {
+      const size_t i = static_cast<size_t>(tile) * E_local + s;
+      const int c = tile_counts[i];
+      tile_counts[i] = running;
+      running += c;
+    }
+  }
+  int total;
+  const int excl = block_exclusive_scan(running, &total);
+  if (s < E_local) offsets[s] = excl;
+  if (s == 0) offsets[E_local] = total;
+}
+
+__global__ __launch_bounds__(kWave) void perm_scatter_kernel(
+    int n_pairs, int k, int E, int E_local, const int32_t* __restrict__ local_experts,
+    const int32_t* __restrict__ topk_idx, const int32_t* __restrict__ tile_prefix,
+    const int32_t* __restrict__ offsets, int32_t* __restrict__ perm_token,
+    int32_t* __restrict__ inv_pos) {
+  extern __shared__ int sm[];
+  int* slot_of = sm;
+  int* next = sm + E;  // next free row of each slot for this tile
+  const int tile = blockIdx.x;
+  for (int s = threadIdx.x; s < E_local; s += kWave)
+    next[s] = offsets[s] + tile_prefix[static_cast<size_t>(tile) * E_local + s];
+  build_slot_map(slot_of, E, E_local, local_experts);
+  const int lane = lane_id();
+  const uint64_t below = (1ull << lane) - 1ull;
+  for (int c0 = tile * kTile; c0 < min(n_pairs, (tile + 1) * kTile); c0 += kWave) {
+    const int p = c0 + lane;
+    int s = -1;
+    if (p < n_pairs) {
+      s = slot_lookup(slot_of, topk_idx[p], E);
+      if (s < 0) inv_pos[p] = -1;
+    }
+    uint64_t pending = __ballot(s >= 0);
+    while (pending) {
+      const int leader = __ffsll(static_cast<long long>(pending)) - 1;
+      const int sl = __shfl(s, leader);
+      const uint64_t same = __ballot(s == sl);
+      const int base = next[sl];
+      if (s == sl) {
+        const int pos = base + __popcll(same & below);
+        perm_token[pos] = p / k;
+        inv_pos[p] = pos;
+      }
+      if (lane == leader) next[sl] = base + __popcll(same);
+      pending &= ~same;
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void gather_rows_kernel(int H, const int32_t* __restrict__ perm_token,
+                                                          const int32_t* __restrict__ n_rows,
+                                                          const uint16_t* __restrict__ x,
+                                                          uint16_t* __restrict__ x_perm) {
+  const int R = *n_rows;
+  const int vpr = H / 8;  // 16-byte vectors per row
+  const int lane = lane_id();
+  const int n_waves = gridDim.x * (blockDim.x / kWave);
+  for (int r = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave; r < R; r += n_waves) {
+    const uint16_t* src = x + static_cast<size_t>(perm_token[r]) * H;
+    uint16_t* dst = x_perm + static_cast<size_t>(r) * H;
+    for (int v = lane; v < vpr; v += kWave) store16(dst + v * 8, load16(src + v * 8));
+  }
+}
+
+}  // namespace
+
+size_t permute_ws_bytes(int T, int k, int E_local) {
+  const size_t n_tiles = static_cast<size_t>(ceil_div(T * k, kTile));
+  return n_tiles * static_cast<size_t>(E_local) * sizeof(int32_t);
+}
+
+hipError_t launch_permute(int T, int k, int E, int E_local, const int32_t* local_experts,
+                          const int32_t* topk_idx, int32_t* offsets, int32_t* perm_token,
+                          int32_t* inv_pos, void* ws, hipStream_t st) {
+  const int n_pairs = T * k;
+  if (n_pairs == 0) return launch_fill_i32(offsets, E_local + 1, 0, st);
+  const int n_tiles = ceil_div(n_pairs, kTile);
+  int32_t* tile_counts = static_cast<int32_t*>(ws);
+  const size_t lds = static_cast<size_t>(E + E_local) * sizeof(int);
+  hipLaunchKernelGGL(perm_count_kernel, dim3(n_tiles), dim3(256), lds, st, n_pairs, E, E_local,
+                     local_experts, topk_idx, tile_counts);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(1024), 0, st, n_tiles, E_local, tile_counts,
+                     offsets);
+  err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(perm_scatter_kernel, dim3(n_tiles), dim3(kWave), lds, st, n_pairs, k, E,
+                     E_local, local_experts, topk_idx, tile_counts, offsets, perm_token, inv_pos);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_rows(int capacity, int H, const int32_t* perm_token, const int32_t* n_rows,
+                              const uint16_t* x, uint16_t* x_perm, hipStream_t st) {
+  if (capacity == 0) return hipSuccess;
+  const int waves_per_block = 4;
+  const int blocks = min(ceil_div(capacity, waves_per_block), 4096);
+  hipLaunchKernelGGL(gather_rows_kernel, dim3(blocks), dim3(waves_per_block * kWave), 0, st, H,
+                     perm_token, n_rows, x, x_perm);
+  return hipGetLastError();
+}
+
+}  // namespace moe

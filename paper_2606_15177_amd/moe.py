@@ -1,0 +1,215 @@
+"""Python binding of the gfx950 MoE-layer library (include/moe.h).
+
+Argument marshalling only: torch tensors are used for device memory and the
+current HIP stream, their raw pointers go to the C ABI, and every step of the
+layer runs in the library's kernels.  Importing this module fails loudly when
+the built library is missing; there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import re
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmoe_gfx950.so")
+HEADER = os.path.join(os.path.dirname(_HERE), "include", "moe.h")
+
+MOE_OK, MOE_ERR_NULL, MOE_ERR_DIMS, MOE_ERR_UNSUPPORTED = 0, -1, -2, -3
+MOE_ERR_WORKSPACE, MOE_ERR_DEVICE, MOE_ERR_ALIGN = -4, -5, -6
+ENTRY_PERMUTE, ENTRY_EXPERT_FFN, ENTRY_FORWARD = 1, 2, 3
+STAGES = ("route", "permute", "ffn_up", "ffn_down", "combine")
+
+
+class MoeDims(C.Structure):
+    _fields_ = [(n, C.c_int32) for n in
+                ("T", "H", "E", "k", "I", "S", "E_local", "n_shared", "I_shared", "flags")]
+
+
+class MoeWeights(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in ("w_gate", "w_up", "w_down", "sh_gate", "sh_up", "sh_down")]
+
+
+class MoeTaps(C.Structure):
+    _fields_ = [("topk_idx", C.c_void_p), ("topk_w", C.c_void_p), ("expert_load", C.c_void_p),
+                ("offsets", C.c_void_p), ("perm_token", C.c_void_p), ("inv_pos", C.c_void_p),
+                ("events", C.c_void_p * (2 * len(STAGES)))]
+
+
+class MoeError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {strerror(status)} ({status})")
+
+
+def _load() -> C.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2606_15177_amd.build`")
+    lib = C.CDLL(LIB_PATH)
+    vp, i32, sz = C.c_void_p, C.c_int, C.c_size_t
+    dp = C.POINTER(MoeDims)
+    sig = {
+        "moe_abi_version": ([], i32),
+        "moe_strerror": ([i32], C.c_char_p),
+        "moe_workspace_bytes": ([dp, i32], sz),
+        "moe_validate": ([dp, i32, sz], i32),
+        "moe_route": ([dp, vp, vp, vp, vp], i32),
+        "moe_route_stats": ([dp, vp, vp, vp, vp, vp], i32),
+        "moe_permute": ([dp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp], i32),
+        "moe_expert_ffn": ([dp, vp, vp, C.POINTER(MoeWeights), vp, vp, vp, vp, sz, vp], i32),
+        "moe_combine": ([dp, vp, vp, vp, vp, vp, vp], i32),
+        "moe_forward": ([dp, vp, vp, vp, vp, C.POINTER(MoeWeights), vp, vp, C.POINTER(MoeTaps),
+                         vp, sz, vp], i32),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = res
+    return lib
+
+
+_lib = _load()
+
+
+def header_functions() -> list[str]:
+    """Names of the functions include/moe.h declares."""
+    with open(HEADER) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(moe_[a-z_]+)\s*\(", text)))
+
+
+def strerror(status: int) -> str:
+    return _lib.moe_strerror(status).decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != MOE_OK:
+        raise MoeError(status, where)
+
+
+def dims(T, H, E, k, I, S, E_local, n_shared=0, I_shared=0, flags=0) -> MoeDims:
+    return MoeDims(T, H, E, k, I, S, E_local, n_shared, I_shared if n_shared else 0, flags)
+
+
+def dims_of(cfg, **override) -> MoeDims:
+    d = dict(cfg.dims)
+    d.update(override)
+    return dims(**d)
+
+
+def workspace_bytes(d: MoeDims, entry: int) -> int:
+    return int(_lib.moe_workspace_bytes(C.byref(d), entry))
+
+
+def validate(d: MoeDims, entry: int = 0, ws_bytes: int = 0) -> int:
+    return int(_lib.moe_validate(C.byref(d), entry, ws_bytes))
+
+
+def _ptr(t, dtypes=None) -> int | None:
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("expected a torch tensor")
+    if not t.is_cuda:
+        raise ValueError("tensor must live on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    if dtypes is not None and t.dtype not in dtypes:
+        raise TypeError(f"dtype {t.dtype} not in {dtypes}")
+    return t.data_ptr()
+
+
+_BF16 = (torch.bfloat16, torch.int16, torch.uint16)
+_I32 = (torch.int32,)
+_I64 = (torch.int64,)
+_F32 = (torch.float32,)
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+
+
+def make_weights(w: dict) -> MoeWeights:
+    return MoeWeights(_ptr(w["w_gate"], _BF16), _ptr(w["w_up"], _BF16), _ptr(w["w_down"], _BF16),
+                      _ptr(w.get("sh_gate"), _BF16), _ptr(w.get("sh_up"), _BF16),
+                      _ptr(w.get("sh_down"), _BF16))
+
+
+def workspace(d: MoeDims, entry: int, device="cuda") -> torch.Tensor:
+    return torch.empty(max(workspace_bytes(d, entry), 1), dtype=torch.uint8, device=device)
+
+
+def route(d, logits, topk_idx, topk_w, stream=None):
+    _check(_lib.moe_route(C.byref(d), _ptr(logits, _F32), _ptr(topk_idx, _I32), _ptr(topk_w, _F32),
+                          _stream(stream)), "moe_route")
+
+
+def route_stats(d, src, topk_idx, counts, expert_load=None, stream=None):
+    _check(_lib.moe_route_stats(C.byref(d), _ptr(src, _I32), _ptr(topk_idx, _I32), _ptr(counts, _I64),
+                                _ptr(expert_load, _I32), _stream(stream)), "moe_route_stats")
+
+
+def permute(d, topk_idx, local_experts, x, offsets, perm_token, inv_pos, x_perm, ws, stream=None):
+    _check(_lib.moe_permute(C.byref(d), _ptr(topk_idx, _I32), _ptr(local_experts, _I32),
+                            _ptr(x, _BF16), _ptr(offsets, _I32), _ptr(perm_token, _I32),
+                            _ptr(inv_pos, _I32), _ptr(x_perm, _BF16), _ptr(ws),
+                            0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)),
+           "moe_permute")
+
+
+def expert_ffn(d, x_perm, offsets, weights, x, y_perm, y_shared, ws, stream=None):
+    w = weights if isinstance(weights, MoeWeights) else make_weights(weights)
+    _check(_lib.moe_expert_ffn(C.byref(d), _ptr(x_perm, _BF16), _ptr(offsets, _I32), C.byref(w),
+                               _ptr(x, _BF16), _ptr(y_perm, _BF16), _ptr(y_shared, _BF16), _ptr(ws),
+                               0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)),
+           "moe_expert_ffn")
+
+
+def combine(d, y_perm, inv_pos, topk_w, y_shared, out, stream=None):
+    _check(_lib.moe_combine(C.byref(d), _ptr(y_perm, _BF16), _ptr(inv_pos, _I32), _ptr(topk_w, _F32),
+                            _ptr(y_shared, _BF16), _ptr(out, _BF16), _stream(stream)), "moe_combine")
+
+
+def make_taps(topk_idx=None, topk_w=None, expert_load=None, offsets=None, perm_token=None,
+              inv_pos=None, events=None) -> MoeTaps:
+    t = MoeTaps(_ptr(topk_idx, _I32), _ptr(topk_w, _F32), _ptr(expert_load, _I32),
+                _ptr(offsets, _I32), _ptr(perm_token, _I32), _ptr(inv_pos, _I32))
+    if events is not None:
+        for i, e in enumerate(events):
+            t.events[i] = e
+    return t
+
+
+def forward(d, logits, src, x, local_experts, weights, counts, out, ws, taps=None, stream=None):
+    w = weights if isinstance(weights, MoeWeights) else make_weights(weights)
+    _check(_lib.moe_forward(C.byref(d), _ptr(logits, _F32), _ptr(src, _I32), _ptr(x, _BF16),
+                            _ptr(local_experts, _I32), C.byref(w), _ptr(counts, _I64),
+                            _ptr(out, _BF16), None if taps is None else C.byref(taps), _ptr(ws),
+                            0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)),
+           "moe_forward")
+
+
+class MoeLayer:
+    """One GPU's MoE layer with its weights resident in HBM.
+
+    Holds the bf16 weights, the placement list and a forward workspace, and
+    calls moe_forward.  ``counts`` (int64 [S, E]) is the caller's source x
+    expert matrix for this layer, accumulated by every call."""
+
+    def __init__(self, d: MoeDims, weights: dict, local_experts=None, device="cuda"):
+        self.d = d
+        self.weights = {k: v for k, v in weights.items() if v is not None}
+        self.local_experts = local_experts
+        self._w = make_weights(self.weights)
+        self.ws = workspace(d, ENTRY_FORWARD, device)
+        self.device = device
+
+    def forward(self, logits, src, x, counts=None, out=None, taps=None, stream=None):
+        if out is None:
+            out = torch.empty((self.d.T, self.d.H), dtype=torch.bfloat16, device=self.device)
+        forward(self.d, logits, src, x, self.local_experts, self._w, counts, out, self.ws, taps, stream)
+        return out

@@ -1,0 +1,106 @@
+"""The C-ABI library without a GPU: it loads, exports every function that
+include/moe.h declares, and its host-side checks return the documented codes
+before touching the device."""
+import ctypes as C
+import subprocess
+
+import pytest
+
+from paper_2606_15177_amd import workloads as W
+
+
+@pytest.fixture(scope="module")
+def moe():
+    from paper_2606_15177_amd import moe
+    return moe
+
+
+def test_exports_every_declared_function(moe):
+    names = moe.header_functions()
+    assert {"moe_route", "moe_route_stats", "moe_permute", "moe_expert_ffn", "moe_combine",
+            "moe_forward", "moe_workspace_bytes", "moe_validate", "moe_strerror"} <= set(names)
+    out = subprocess.run(["nm", "-D", "--defined-only", moe.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if line.strip()}
+    for n in names:
+        assert n in exported, n
+    lib = C.CDLL(moe.LIB_PATH)
+    for n in names:
+        getattr(lib, n)
+
+
+def test_abi_version_and_strerror(moe):
+    assert moe._lib.moe_abi_version() == 1
+    for code in (0, -1, -2, -3, -4, -5, -6):
+        assert moe.strerror(code) and moe.strerror(code) != "unknown status"
+    assert moe.strerror(-99) == "unknown status"
+
+
+@pytest.mark.parametrize("name", W.CONFIG_ORDER)
+def test_configs_validate(moe, name):
+    d = moe.dims_of(W.CONFIGS[name])
+    assert moe.validate(d) == moe.MOE_OK
+    for entry in (moe.ENTRY_PERMUTE, moe.ENTRY_EXPERT_FFN, moe.ENTRY_FORWARD):
+        need = moe.workspace_bytes(d, entry)
+        assert need > 0 and need % 256 == 0
+        assert moe.validate(d, entry, need) == moe.MOE_OK
+        assert moe.validate(d, entry, need - 1) == moe.MOE_ERR_WORKSPACE
+
+
+def test_forward_workspace_size(moe):
+    cfg = W.CONFIGS["ep_share_dsv3"]
+    d = moe.dims_of(cfg)
+    rows = cfg.T * cfg.k
+    # x_perm + y_perm + h dominate: capacity T*k rows
+    lower = rows * cfg.H * 2 * 2 + rows * cfg.I * 2
+    assert lower <= moe.workspace_bytes(d, moe.ENTRY_FORWARD) < lower * 1.2
+
+
+@pytest.mark.parametrize("change,code", [
+    (dict(T=-1), -2), (dict(H=0), -2), (dict(k=0), -2), (dict(k=9), -2), (dict(S=0), -2),
+    (dict(E_local=0), -2), (dict(E_local=9), -2), (dict(n_shared=-1), -2),
+    (dict(n_shared=1, I_shared=0), -2), (dict(I=0), -2),
+    (dict(H=12), -3), (dict(I=100), -3), (dict(n_shared=1, I_shared=36), -3),
+    (dict(E=1025, E_local=8), -3), (dict(E=64, k=33), -3), (dict(flags=1), -3),
+    (dict(T=2 ** 30, k=2), -3),
+])
+def test_validate_rejects(moe, change, code):
+    base = dict(T=16, H=64, E=8, k=2, I=64, S=2, E_local=8, n_shared=0, I_shared=0)
+    base.update(change)
+    flags = base.pop("flags", 0)
+    d = moe.dims(**base, flags=flags)
+    assert moe.validate(d) == code
+    assert moe.workspace_bytes(d, moe.ENTRY_FORWARD) == 0
+
+
+def test_entry_points_reject_before_launch(moe):
+    """Errors are decided on the host; nothing reaches the device."""
+    lib = moe._lib
+    d = moe.dims(T=4, H=64, E=8, k=2, I=64, S=2, E_local=4)
+    assert lib.moe_route(None, None, None, None, None) == moe.MOE_ERR_NULL
+    assert lib.moe_route(C.byref(d), None, None, None, None) == moe.MOE_ERR_NULL
+    assert lib.moe_route_stats(C.byref(d), None, None, None, None, None) == moe.MOE_ERR_NULL
+    # no placement list while E_local < E
+    assert lib.moe_permute(C.byref(d), 16, None, None, 16, 16, 16, None, None, 0, None) == moe.MOE_ERR_DIMS
+    d8 = moe.dims(T=4, H=64, E=8, k=2, I=64, S=2, E_local=8)
+    # x given without x_perm
+    assert lib.moe_permute(C.byref(d8), 16, None, 16, 16, 16, 16, None, None, 0, None) == moe.MOE_ERR_NULL
+    # misaligned x
+    assert lib.moe_permute(C.byref(d8), 16, None, 24, 16, 16, 16, 32, None, 0, None) == moe.MOE_ERR_ALIGN
+    # workspace too small
+    assert lib.moe_permute(C.byref(d8), 16, None, 16, 16, 16, 16, 32, 256, 0, None) == moe.MOE_ERR_WORKSPACE
+    w = moe.MoeWeights(None, None, None, None, None, None)
+    assert lib.moe_expert_ffn(C.byref(d8), 16, 16, C.byref(w), None, 16, None, None, 0, None) == moe.MOE_ERR_NULL
+    w = moe.MoeWeights(16, 16, 24, None, None, None)
+    assert lib.moe_expert_ffn(C.byref(d8), 16, 16, C.byref(w), None, 16, None, None, 0, None) == moe.MOE_ERR_ALIGN
+    w = moe.MoeWeights(16, 16, 16, None, None, None)
+    dsh = moe.dims(T=4, H=64, E=8, k=2, I=64, S=2, E_local=8, n_shared=1, I_shared=64)
+    assert lib.moe_expert_ffn(C.byref(dsh), 16, 16, C.byref(w), None, 16, None, None, 0, None) == moe.MOE_ERR_NULL
+    assert lib.moe_combine(C.byref(d8), None, 16, 16, None, 16, None) == moe.MOE_ERR_NULL
+    assert lib.moe_forward(C.byref(d8), 16, None, 16, None, C.byref(w), 16, 16, None, None, 0,
+                           None) == moe.MOE_ERR_NULL       # counts without src
+    ws_need = moe.workspace_bytes(d8, moe.ENTRY_FORWARD)
+    assert lib.moe_forward(C.byref(d8), 16, 16, 16, None, C.byref(w), 16, 16, None, 256, ws_need - 1,
+                           None) == moe.MOE_ERR_WORKSPACE
+    assert lib.moe_forward(C.byref(d8), 16, 16, 16, None, C.byref(w), 16, 16, None, 128, ws_need,
+                           None) == moe.MOE_ERR_ALIGN      # workspace not 256-byte aligned

@@ -1,0 +1,147 @@
+"""Whole-layer GPU parity (moe_forward) against the CPU oracle: every
+intermediate the layer exposes bit-exact (expert ids, counts, offsets,
+dispatch order), gates within 1e-6 and the output within the layer
+tolerance; at the five workloads' full sizes the output is checked on sampled
+tokens, each computed by the oracle from the definition."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle
+from paper_2606_15177_amd import workloads as W
+from tests.gpu_util import (assert_gates_close, assert_layer_close, dev, dev_weights, host_bf16,
+                            sample_tokens, workload)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def moe():
+    from paper_2606_15177_amd import moe
+    return moe
+
+
+def _forward(moe, cfg, wl, counts=None, repeat=1):
+    d = moe.dims_of(cfg)
+    T, k = cfg.T, cfg.k
+    taps_t = dict(topk_idx=torch.full((max(T, 1), k), -9, dtype=torch.int32, device="cuda"),
+                  topk_w=torch.zeros((max(T, 1), k), dtype=torch.float32, device="cuda"),
+                  expert_load=torch.full((cfg.E,), -9, dtype=torch.int32, device="cuda"),
+                  offsets=torch.full((cfg.E_local + 1,), -9, dtype=torch.int32, device="cuda"),
+                  perm_token=torch.full((max(T * k, 1),), -9, dtype=torch.int32, device="cuda"),
+                  inv_pos=torch.full((max(T * k, 1),), -9, dtype=torch.int32, device="cuda"))
+    taps = moe.make_taps(**taps_t)
+    loc = None if wl["local_experts"] is None else dev(wl["local_experts"])
+    layer = moe.MoeLayer(d, dev_weights(wl), loc)
+    if counts is None:
+        counts = torch.zeros((cfg.S, cfg.E), dtype=torch.int64, device="cuda")
+    logits, src, x = dev(wl["logits"]), dev(wl["src"]), dev(wl["x"])
+    outs = []
+    for _ in range(repeat):
+        out = torch.full((max(T, 1), cfg.H), 3.0, dtype=torch.bfloat16, device="cuda")
+        layer.forward(logits, src, x, counts, out[:T] if T else None, taps)
+        outs.append(out)
+    torch.cuda.synchronize()
+    res = {n: t.cpu().numpy() for n, t in taps_t.items()}
+    res["counts"] = counts.cpu().numpy()
+    res["outs"] = [host_bf16(o)[:T] for o in outs]
+    return res
+
+
+def _check_routing(cfg, wl, res, calls=1):
+    T, k = cfg.T, cfg.k
+    ridx, rw = oracle.route(wl["logits"], k)
+    np.testing.assert_array_equal(res["topk_idx"][:T], ridx)
+    assert_gates_close(res["topk_w"][:T], rw, cfg.name)
+    rc, rl = oracle.route_stats(wl["src"], ridx, cfg.S, cfg.E)
+    np.testing.assert_array_equal(res["counts"], calls * rc)
+    np.testing.assert_array_equal(res["expert_load"], rl)
+    off, perm, inv = oracle.permute(ridx, cfg.E, cfg.E_local, wl["local_experts"])
+    np.testing.assert_array_equal(res["offsets"], off)
+    np.testing.assert_array_equal(res["perm_token"][: off[-1]], perm)
+    np.testing.assert_array_equal(res["inv_pos"][: T * k], inv)
+    return ridx
+
+
+def test_forward_tiny_all_tokens_and_determinism(moe):
+    cfg = W.CONFIGS["tiny"]
+    wl = workload("tiny")
+    res = _forward(moe, cfg, wl, repeat=2)
+    _check_routing(cfg, wl, res, calls=2)
+    ref = oracle.forward_tokens(cfg.dims, np.arange(cfg.T), wl["logits"], wl["x"], wl["local_experts"], wl)
+    assert_layer_close(res["outs"][0], ref, "tiny")
+    np.testing.assert_array_equal(res["outs"][0], res["outs"][1])     # bitwise deterministic
+
+
+@pytest.mark.parametrize("variant", [
+    dict(T=1), dict(T=2, k=1), dict(T=64, E=16, k=4, E_local=5, local_layout="choice"),
+    dict(T=63, H=136, I=200, n_shared=2, I_shared=72), dict(T=300, H=200, I=136, E=12, k=3, E_local=12),
+    dict(T=777, E=33, k=5, E_local=7, local_layout="choice", n_shared=1, I_shared=64),
+    dict(T=100, src_layout="blocks"), dict(T=100, src_layout="interleaved", S=3),
+])
+def test_forward_variants(moe, variant):
+    cfg = W.CONFIGS["tiny"].replace(name="variant", **variant)
+    wl = W.make_workload(cfg, seed=2)
+    res = _forward(moe, cfg, wl)
+    _check_routing(cfg, wl, res)
+    ref = oracle.forward_tokens(cfg.dims, np.arange(cfg.T), wl["logits"], wl["x"], wl["local_experts"], wl)
+    assert_layer_close(res["outs"][0], ref, str(variant))
+
+
+def test_forward_tokens_without_local_experts(moe):
+    """Tokens none of whose experts are hosted here get only the shared part;
+    without shared experts they get exact zeros."""
+    cfg = W.CONFIGS["tiny"].replace(name="remote", E=16, k=2, E_local=2, local_layout="choice", T=200)
+    wl = W.make_workload(cfg, seed=3)
+    res = _forward(moe, cfg, wl)
+    ridx = _check_routing(cfg, wl, res)
+    local = set(wl["local_experts"].tolist())
+    remote_tok = [t for t in range(cfg.T) if not (set(ridx[t].tolist()) & local)]
+    assert remote_tok
+    assert (res["outs"][0][remote_tok] == 0).all()
+    ref = oracle.forward_tokens(cfg.dims, np.arange(cfg.T), wl["logits"], wl["x"], wl["local_experts"], wl)
+    assert_layer_close(res["outs"][0], ref, "remote")
+
+
+def test_forward_one_hot_gates_is_dense_ffn(moe):
+    cfg = W.CONFIGS["tiny"].replace(name="onehot", T=100, E=8, k=2)
+    wl = W.make_workload(cfg, seed=4)
+    chosen = np.random.default_rng(0).integers(0, cfg.E, cfg.T)
+    logits = np.full((cfg.T, cfg.E), -np.inf, np.float32)
+    logits[np.arange(cfg.T), chosen] = 0.0
+    wl["logits"] = logits
+    res = _forward(moe, cfg, wl)
+    ref = np.stack([oracle.swiglu_ffn(wl["x"][t], wl["w_gate"][e], wl["w_up"][e], wl["w_down"][e])
+                    for t, e in enumerate(chosen)])
+    assert_layer_close(res["outs"][0], ref, "one-hot")
+
+
+def test_forward_empty_batch(moe):
+    cfg = W.CONFIGS["tiny"].replace(name="empty", T=0)
+    wl = W.make_workload(cfg, seed=0)
+    d = moe.dims_of(cfg)
+    layer = moe.MoeLayer(d, dev_weights(wl))
+    counts = torch.zeros((cfg.S, cfg.E), dtype=torch.int64, device="cuda")
+    moe.forward(d, None, None, None, None, layer._w, counts, None, layer.ws)
+    torch.cuda.synchronize()
+    assert counts.sum().item() == 0
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", W.CONFIG_ORDER)
+def test_forward_full_size(moe, name):
+    """Every routing intermediate over all tokens, and the output on sampled
+    tokens, at the workload's full size and in the bench's launch configuration."""
+    cfg = W.CONFIGS[name]
+    wl = workload(name)
+    res = _forward(moe, cfg, wl)
+    ridx = _check_routing(cfg, wl, res)
+    n = {"decode_mixtral": 12, "ep_share_dsv3": 12}.get(name, 24)
+    extra = []
+    if wl["local_experts"] is not None:    # include tokens that have no local expert
+        local = set(wl["local_experts"].tolist())
+        extra = [t for t in range(cfg.T) if not (set(ridx[t].tolist()) & local)][:2]
+    toks = sample_tokens(cfg.T, n, seed=1, extra=extra)
+    ref = oracle.forward_tokens(cfg.dims, toks, wl["logits"], wl["x"], wl["local_experts"], wl)
+    e = assert_layer_close(res["outs"][0][toks], ref, name)
+    print(f"{name}: rel {e['rel']:.2e} mae {e['mae']:.2e} rel_mae {e['rel_mae']:.2e}")
