@@ -1,84 +1,39 @@
 // Expert FFN for decode-sized batches: weight streaming.
 //
 // With at most a few dozen rows per expert the grouped GEMM is bound by
-// reading the experts' weights from HBM once.  The weights therefore take
-// the MFMA's 32-row A operand and the (few) tokens its 32-column B operand:
+// reading the active experts' weights from HBM exactly once.  The weights take
+// the MFMA's 32-row A operand and the tokens its 32-column B operand:
 // v_mfma_f32_32x32x16_bf16 computes C[n][t] += W[n][k] X[t][k].
 //
-// Work split: one workgroup per (expert group, 32 weight rows); its 4 waves
-// split the K range; every lane streams 128 contiguous bytes of one weight
-// row per step (eight 16-byte loads, prefetched one step ahead), so each
-// weight byte is read exactly once and every 128-byte line is consumed by a
-// single lane.  The reduction over K runs in the same lane order in both
-// operands, so lane l can hold k in [64*(l/32), 64*(l/32)+64) of the step:
-// the MFMA sums over whichever 16 k values the two operands hold in common.
-// Partial sums of waves 1..3 are reduced into wave 0 through LDS; wave 0 runs
-// the epilogue (SwiGLU for the gate/up pair) and writes bf16.
+// Work split: one workgroup per (expert group, 32 weight rows).  Its
+// NMAT*KP waves are autonomous: wave w streams matrix w / KP (gate or up, or
+// the single down matrix) over K part w % KP, in steps of KS elements.  Each
+// step is loaded with row-contiguous 16-byte vectors (KS/8 lanes cover one
+// row's segment, so every request is a full run of 128-byte lines) into a
+// register ring DEPTH steps deep, then transposed through the wave's own LDS
+// region into the MFMA operand layout (16-byte slot c of row r stored at
+// c ^ (r mod KS/8), so the 32 rows read by one fragment spread over the
+// banks).  No workgroup barrier is taken inside the K loop; one barrier at the
+// end reduces the K parts (fixed order, deterministic) and applies SwiGLU.
+// Each workgroup starts its K walk at a rotated step so that concurrently
+// running workgroups, whose rows sit H*2 bytes apart, spread over the HBM
+// channels instead of queueing on the same ones.
 #include "common.h"
 #include "ffn_impl.h"
 
 namespace moe {
 namespace {
 
-constexpr int kWaves = 4;
-constexpr int kStepK = 128;  // K elements per wave step (64 per lane half)
+template <int NMAT, int KP, int KS, int DEPTH>
+__global__ __launch_bounds__(NMAT* KP* kWave) void skinny_kernel(GemmArgs a) {
+  constexpr int W = NMAT * KP;
+  constexpr int ROWB = KS * 2;          // bytes of one row segment
+  constexpr int PPR = KS / 8;           // 16-byte pieces per row segment
+  constexpr int CPL = 32 * PPR / kWave; // pieces per lane per step
+  constexpr int KK = KS / 16;           // MFMA k-steps per step
+  static_assert(CPL >= 1 && (kWave % PPR) == 0, "step shape");
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
-template <int NCH, bool GATED>
-struct StepRegs {
-  u32x4 w0[8];
-  u32x4 w1[GATED ? 8 : 1];
-  u32x4 x[NCH][8];
-};
-
-template <int NCH, bool GATED>
-__device__ __forceinline__ void load_step(StepRegs<NCH, GATED>& r, const GemmArgs& a, int g,
-                                          int wrow, bool wrow_ok, int row_base, int tok0, int m,
-                                          int kb) {
-  const int lane = lane_id();
-  const int k_lane = kb * kStepK + (lane >> 5) * 64;  // first k of this lane's slice
-  const size_t gbase = static_cast<size_t>(g) * a.group_stride;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int kk = k_lane + 8 * j;
-    const bool kok = kk < a.K;
-    size_t off = 0;
-    if (kok) off = gbase + weight_col_offset(a, kk) + static_cast<size_t>(wrow) * a.ldw;
-    const u32x4 zero = {0u, 0u, 0u, 0u};
-    r.w0[j] = (kok && wrow_ok) ? load16_nt(a.w0 + off) : zero;
-    if constexpr (GATED) r.w1[j] = (kok && wrow_ok) ? load16_nt(a.w1 + off) : zero;
-  }
-#pragma unroll
-  for (int ch = 0; ch < NCH; ++ch) {
-    const int tok = tok0 + ch * 32 + (lane & 31);
-    const bool tok_ok = tok < m;
-    const uint16_t* px = a.x + static_cast<size_t>(row_base + (tok_ok ? tok : 0)) * a.K;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int kk = k_lane + 8 * j;
-      const u32x4 zero = {0u, 0u, 0u, 0u};
-      r.x[ch][j] = (tok_ok && kk < a.K) ? load16(px + kk) : zero;
-    }
-  }
-}
-
-template <int NCH, bool GATED>
-__device__ __forceinline__ void mma_step(const StepRegs<NCH, GATED>& r, f32x16 (&acc0)[NCH],
-                                         f32x16 (&acc1)[NCH]) {
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-#pragma unroll
-    for (int ch = 0; ch < NCH; ++ch) {
-      acc0[ch] = mfma32x32x16(as_bf16x8(r.w0[j]), as_bf16x8(r.x[ch][j]), acc0[ch]);
-      if constexpr (GATED)
-        acc1[ch] = mfma32x32x16(as_bf16x8(r.w1[j]), as_bf16x8(r.x[ch][j]), acc1[ch]);
-    }
-  }
-}
-
-template <int NCH, bool GATED>
-__global__ __launch_bounds__(kWaves * kWave) void skinny_kernel(GemmArgs a) {
-  constexpr int kMats = GATED ? 2 : 1;
-  __shared__ float red[kWaves - 1][kMats][NCH][16][kWave];
   const int g = blockIdx.y;
   int row_base = 0, m = a.static_rows;
   if (a.offsets) {
@@ -86,57 +41,107 @@ __global__ __launch_bounds__(kWaves * kWave) void skinny_kernel(GemmArgs a) {
     m = a.offsets[g + 1] - row_base;
   }
   if (m <= 0) return;  // an expert with no rows costs no weight traffic
-  const int wave = threadIdx.x / kWave;
-  const int lane = lane_id();
-  const int n0 = blockIdx.x * 32;
-  const int wrow = n0 + (lane & 31);
-  const bool wrow_ok = wrow < a.N;
-  const int nkb = ceil_div(a.K, kStepK);
-  const int kb0 = wave * nkb / kWaves;
-  const int kb1 = (wave + 1) * nkb / kWaves;
 
-  for (int tok0 = 0; tok0 < m; tok0 += 32 * NCH) {
-    f32x16 acc0[NCH], acc1[NCH];
+  const int tid = threadIdx.x, wave = tid / kWave, lane = lane_id();
+  const int mat = wave / KP, part = wave % KP;
+  const int n0 = blockIdx.x * 32;
+  const int nks = ceil_div(a.K, KS);
+  const int q0 = part * nks / KP, q1 = (part + 1) * nks / KP;
+  const int nq = q1 - q0;
+  const int rot = nq > 0 ? static_cast<int>((blockIdx.x * 7u + blockIdx.y * 3u) % nq) : 0;
+  unsigned char* wl = smem + wave * (32 * ROWB);
+
+  const uint16_t* wbase = (mat == 0 ? a.w0 : a.w1) + static_cast<size_t>(g) * a.group_stride;
+  const int p_l = lane % PPR;
+  size_t roff[CPL];
+  int dst[CPL];
+  bool rok[CPL];
 #pragma unroll
-    for (int ch = 0; ch < NCH; ++ch) {
-      acc0[ch] = f32x16{};
-      acc1[ch] = f32x16{};
+  for (int i = 0; i < CPL; ++i) {
+    const int r = lane / PPR + (kWave / PPR) * i;
+    rok[i] = n0 + r < a.N;
+    roff[i] = static_cast<size_t>(rok[i] ? n0 + r : 0) * a.ldw;
+    dst[i] = r * ROWB + ((p_l ^ (r & (PPR - 1))) << 4);
+  }
+
+  auto kstep = [&](int j) {
+    int s = rot + j;
+    if (s >= nq) s -= nq;
+    return q0 + s;
+  };
+
+  for (int tok0 = 0; tok0 < m; tok0 += 64) {
+    const int mc = min(64, m - tok0);
+    const int nch = mc > 32 ? 2 : 1;
+    const uint16_t* xrow[2];
+    bool tok_ok[2];
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int tok = tok0 + c * 32 + (lane & 31);
+      tok_ok[c] = c < nch && tok < m;
+      xrow[c] = a.x + static_cast<size_t>(row_base + (tok_ok[c] ? tok : 0)) * a.K + 8 * (lane >> 5);
     }
-    if (kb0 < kb1) {
-      StepRegs<NCH, GATED> cur, nxt;
-      load_step<NCH, GATED>(cur, a, g, wrow, wrow_ok, row_base, tok0, m, kb0);
-      for (int kb = kb0; kb < kb1; ++kb) {
-        if (kb + 1 < kb1) load_step<NCH, GATED>(nxt, a, g, wrow, wrow_ok, row_base, tok0, m, kb + 1);
-        mma_step<NCH, GATED>(cur, acc0, acc1);
-        cur = nxt;
+
+    u32x4 st[DEPTH][CPL];
+    f32x16 acc[2] = {f32x16{}, f32x16{}};
+    auto gload = [&](u32x4 (&s)[CPL], int kb) {
+      const int kk = kb * KS + p_l * 8;
+      const bool kok = kk < a.K;
+      const size_t col = kok ? weight_col_offset(a, kk) : 0;
+      const u32x4 zero = {0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int i = 0; i < CPL; ++i) s[i] = (rok[i] && kok) ? load16(wbase + roff[i] + col) : zero;
+    };
+
+#pragma unroll
+    for (int s = 0; s < DEPTH; ++s)
+      if (s < nq) gload(st[s], kstep(s));
+    for (int j0 = 0; j0 < nq; j0 += DEPTH) {
+#pragma unroll
+      for (int u = 0; u < DEPTH; ++u) {
+        const int j = j0 + u;
+        if (j < nq) {
+          const int kb = kstep(j);
+          u32x4 xt[2][KK];
+#pragma unroll
+          for (int c = 0; c < 2; ++c)
+#pragma unroll
+            for (int kk = 0; kk < KK; ++kk) {
+              const int k = kb * KS + 16 * kk + 8 * (lane >> 5);
+              const u32x4 zero = {0u, 0u, 0u, 0u};
+              xt[c][kk] = (tok_ok[c] && k < a.K) ? load16(xrow[c] + kb * KS + 16 * kk) : zero;
+            }
+#pragma unroll
+          for (int i = 0; i < CPL; ++i) *reinterpret_cast<u32x4*>(wl + dst[i]) = st[u][i];
+          if (j + DEPTH < nq) gload(st[u], kstep(j + DEPTH));
+#pragma unroll
+          for (int kk = 0; kk < KK; ++kk) {
+            const int p = 2 * kk + (lane >> 5);
+            const int row = lane & 31;
+            const u32x4 wv =
+                *reinterpret_cast<const u32x4*>(wl + row * ROWB + ((p ^ (row & (PPR - 1))) << 4));
+            acc[0] = mfma32x32x16(as_bf16x8(wv), as_bf16x8(xt[0][kk]), acc[0]);
+            if (nch > 1) acc[1] = mfma32x32x16(as_bf16x8(wv), as_bf16x8(xt[1][kk]), acc[1]);
+          }
+        }
       }
     }
-    // reduce the K-split partial sums into wave 0
-    if (wave > 0) {
+
+    // reduce the K parts in a fixed order; wave 0 applies the epilogue
+    __syncthreads();
+    float* red = reinterpret_cast<float*>(smem);
 #pragma unroll
-      for (int ch = 0; ch < NCH; ++ch)
+    for (int c = 0; c < 2; ++c)
+      if (c < nch)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          red[wave - 1][0][ch][v][lane] = acc0[ch][v];
-          if constexpr (GATED) red[wave - 1][kMats - 1][ch][v][lane] = acc1[ch][v];
-        }
-    }
+        for (int v = 0; v < 16; ++v) red[((wave * 2 + c) * 16 + v) * kWave + lane] = acc[c][v];
     __syncthreads();
     if (wave == 0) {
-#pragma unroll
-      for (int w = 0; w < kWaves - 1; ++w)
-#pragma unroll
-        for (int ch = 0; ch < NCH; ++ch)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            acc0[ch][v] += red[w][0][ch][v][lane];
-            if constexpr (GATED) acc1[ch][v] += red[w][kMats - 1][ch][v][lane];
-          }
       // lane holds C[n = 8*(v/4) + 4*(lane/32) + v%4][t = lane%32] of each chunk
 #pragma unroll
-      for (int ch = 0; ch < NCH; ++ch) {
-        const int tok = tok0 + ch * 32 + (lane & 31);
-        if (tok >= m) continue;
+      for (int c = 0; c < 2; ++c) {
+        const int tok = tok0 + c * 32 + (lane & 31);
+        if (c >= nch || tok >= m) continue;
         uint16_t* orow = a.out + static_cast<size_t>(row_base + tok) * a.N;
 #pragma unroll
         for (int v4 = 0; v4 < 4; ++v4) {
@@ -145,8 +150,12 @@ __global__ __launch_bounds__(kWaves * kWave) void skinny_kernel(GemmArgs a) {
           float o[4];
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const float c0 = acc0[ch][4 * v4 + i];
-            o[i] = GATED ? silu(c0) * acc1[ch][4 * v4 + i] : c0;
+            const int v = 4 * v4 + i;
+            float s0 = 0.f, s1 = 0.f;
+            for (int p = 0; p < KP; ++p) s0 += red[((p * 2 + c) * 16 + v) * kWave + lane];
+            if (NMAT == 2)
+              for (int p = 0; p < KP; ++p) s1 += red[(((KP + p) * 2 + c) * 16 + v) * kWave + lane];
+            o[i] = NMAT == 2 ? silu(s0) * s1 : s0;
           }
           uint2 pk;
           pk.x = pack_bf16x2(o[0], o[1]);
@@ -159,20 +168,28 @@ __global__ __launch_bounds__(kWaves * kWave) void skinny_kernel(GemmArgs a) {
   }
 }
 
-template <int NCH, bool GATED>
+template <int NMAT, int KP, int KS, int DEPTH>
 hipError_t launch_skinny_t(const Segments& seg, const GemmArgs& a, hipStream_t st) {
+  constexpr int W = NMAT * KP;
+  constexpr size_t kLds = (32 * KS * 2 > 2 * 16 * kWave * 4) ? W * 32 * KS * 2 : W * 2 * 16 * kWave * 4;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&skinny_kernel<NMAT, KP, KS, DEPTH>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kLds));
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
   dim3 grid(ceil_div(a.N, 32), seg.groups);
-  hipLaunchKernelGGL((skinny_kernel<NCH, GATED>), grid, dim3(kWaves * kWave), 0, st, a);
+  hipLaunchKernelGGL((skinny_kernel<NMAT, KP, KS, DEPTH>), grid, dim3(W * kWave), kLds, st, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_skinny(const Segments& seg, const GemmArgs& a, bool gated, hipStream_t st) {
-  // chunks of 32 tokens held at once; more rows are handled by re-streaming
-  if (seg.max_rows <= 32)
-    return gated ? launch_skinny_t<1, true>(seg, a, st) : launch_skinny_t<1, false>(seg, a, st);
-  return gated ? launch_skinny_t<2, true>(seg, a, st) : launch_skinny_t<2, false>(seg, a, st);
+  // gate/up: 2 matrices x 4 K parts, 64-wide steps; down: 8 K parts, 128-wide
+  // steps (the measured best shapes for the decode workload)
+  return gated ? launch_skinny_t<2, 4, 64, 2>(seg, a, st) : launch_skinny_t<1, 8, 128, 2>(seg, a, st);
 }
 
 }  // namespace moe
