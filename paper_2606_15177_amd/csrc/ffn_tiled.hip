@@ -1,110 +1,118 @@
-// Expert FFN for prefill-sized batches: a persistent, LDS-tiled bf16 MFMA
-// grouped GEMM.
+// Expert FFN for prefill-sized batches: a persistent bf16 MFMA grouped GEMM
+// with direct-to-LDS loads and two ping-pong wave groups.
 //
-// Output tiles are BM token rows x BN weight rows of one group (expert).  The
-// tile list is implied by the device-side offsets: every workgroup computes
-// the per-group prefix of ceil(rows/BM) once, then walks tile ids
-// blockIdx', blockIdx'+gridDim, ... where blockIdx' renumbers workgroups so
-// that each XCD (workgroups are dealt round-robin to the 8 XCDs) owns a
-// contiguous run of tiles: consecutive tiles share the token rows and, within
-// one expert, the weights, which keeps them in that XCD's L2.  Group sizes
-// never leave the device.
+// Tiles.  An output tile is 256 token rows x 256 weight rows of one group
+// (expert).  For the gate/up GEMM the 256 weight rows are 128 gate rows and
+// the 128 up rows of the same output columns, so a tile yields 128 columns of
+// h = silu(gate) * up.  The tile list is implied by the device-side offsets:
+// every workgroup computes the per-group prefix of ceil(rows/256) once, then
+// walks tile ids t, t+gridDim, ... where t renumbers workgroups so that each
+// XCD (workgroups are dealt round-robin to the 8 XCDs) owns a contiguous run
+// of tiles.  Tiles are numbered group-major, then by n-tile, then by m-tile,
+// so the m-tiles that share a weight tile run side by side on one XCD and
+// the weights are fetched from HBM once.  Group sizes never leave the
+// device.
 //
-// K loop: BK = 64.  Each K-block of X (BM x 64) and W (BN x 64) is loaded
-// with 16-byte vectors into registers, then stored to one of two LDS buffers
-// (row = 128 bytes, 16-byte chunk c of row r stored at slot c ^ swz(r), so
-// the MFMA fragment reads spread over all banks).  The
-// load of block kb+1 is in flight while block kb feeds the MFMAs.
+// Stages.  K advances in stages of 32.  A stage holds X[256 x 32] and
+// W[256 x 32] in LDS (64-byte rows, 32 KB) and is filled by
+// buffer_load_dwordx4 ... lds, which writes 64 lanes x 16 bytes to
+// consecutive LDS addresses without passing through registers.  Four stages
+// form a ring: the loads of stage j+3 are issued while stage j is consumed,
+// so a load has about three stage times to arrive, and the stage sequence
+// runs on across tile boundaries (the next tile's first stages are in flight
+// during a tile's last ones).  Chunk c (16 bytes) of LDS row r sits at slot
+// c ^ ((r >> 2) & 3): every lane of a load fetches the global chunk that
+// belongs at its fixed LDS slot, and the 16 rows that 16 lanes of an MFMA
+// fragment read land in 16 distinct bank groups.  Rows past a group's end,
+// columns past N and the K tail get byte offsets >= 2^31, past the buffer
+// descriptor's range: they read as zeros and cost no memory traffic.
 //
-// MFMA v_mfma_f32_32x32x16_bf16 with the weights as the A operand and tokens
-// as B: C[n][t]; lane l then holds 4 consecutive output columns of token
-// l % 32 in each group of 4 accumulators, written as one 8-byte store.  For
-// the gate/up GEMM the BN weight rows of a wave are its WTN/2 gate rows
-// followed by the WTN/2 up rows of the same columns, so each lane holds
-// gate and up for the same (token, column) and applies SwiGLU in registers.
+// Ping-pong.  The 8 waves form two groups of four, one wave of each group
+// per SIMD.  Group 0 computes token rows 0..127 of the tile and group 1 rows
+// 128..255; a wave owns 64 token rows x 128 weight rows (2 x 4 MFMA tiles of
+// v_mfma_f32_32x32x16_bf16, weights as the A operand, tokens as B).  The two
+// groups alternate, one phase apart, between a memory phase (issue loads,
+// read the stage's fragments from LDS into registers) and a compute phase
+// (16 MFMAs on registers only), with a workgroup barrier between phases: on
+// every SIMD one wave issues MFMAs while the other one feeds LDS.
+//
+// Waits.  Each wave issues the loads of stage j+3 for its part in its memory
+// phase of stage j and waits for its own loads of stage j+1 (s_waitcnt vmcnt
+// with the two younger stages' 8 loads still in flight) before the barrier
+// that precedes the first read of stage j+1; it waits for its LDS reads
+// (lgkmcnt(0)) before every barrier, so a buffer is refilled only after both
+// groups have read it.
 #include "ffn_impl.h"
 
 namespace moe {
 namespace {
 
-constexpr int kBK = 64;
+constexpr int kBM = 256;                          // token rows per tile
+constexpr int kBN = 256;                          // weight rows per tile
+constexpr int kBK = 32;                           // K per stage
+constexpr int kStages = 4;                        // LDS ring depth
+constexpr int kThreads = 8 * kWave;
+constexpr int kRowBytes = kBK * 2;                // 64
+constexpr int kPartBytes = kBM * kRowBytes;       // one operand of a stage: 16 KB
+constexpr int kStageBytes = 2 * kPartBytes;       // X part, then W part
+constexpr int kLdsBytes = kStages * kStageBytes;  // 128 KB
+constexpr int kLoadsPerStage = 4;                 // per wave: 4 loads of 1 KB (group 0: X, group 1: W)
 constexpr int kMaxGroups = 1024;
+static_assert(kBM == kBN && kBM * kRowBytes == 16 * 1024 * 1, "a stage part is 16 loads of 1 KB");
 
-// LDS slot key of a 128-byte row: chunk c of row r is stored in slot
-// c ^ swz(r).  Among any 16 consecutive rows, each run of 8 and each set of 8
-// same-parity rows gets 8 distinct keys, so the 16-byte fragment reads of an
-// MFMA operand are bank-conflict free whether the LDS serves 8 or 16 lanes of
-// 16 bytes per cycle.  The key depends on r mod 16 only, so writers (which
-// know a row modulo their staging stride) and readers (modulo 32) agree.
-__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+// s_waitcnt immediates (gfx9 layout: vmcnt [3:0] and [15:14], expcnt [6:4],
+// lgkmcnt [11:8]); a field at its maximum does not wait.
+constexpr int wait_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+constexpr int kWaitLgkm0 = 15 | (3 << 14) | (7 << 4);
+constexpr int kWaitAll = 0;
 
-// Issue order of one K-block, as scheduling-group constraints on MFMA index
-// m = 0..S*P-1 (S steps of P MFMAs, F fragment reads per step): after each
-// MFMA, the next step's fragment reads spread evenly over the step; the L
-// global loads of the next K-block spread over the first half of the MFMAs
-// and its Wn LDS stores over the second half.  The matrix cores are fed
-// continuously instead of idling through a load/store burst each block.
-template <int m, int S, int P, int F, int L, int Wn>
-__device__ __forceinline__ void sched_mfma_seq() {
-  if constexpr (m < S * P) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-    constexpr int step = m / P, j = m % P;
-    if constexpr (step + 1 < S) {
-      constexpr int r0 = F * j / P, r1 = F * (j + 1) / P;
-      if constexpr (r1 > r0) __builtin_amdgcn_sched_group_barrier(0x100, r1 - r0, 0);  // LDS reads
-    }
-    constexpr int H = S * P / 2;
-    if constexpr (m < H) {
-      constexpr int a = L * m / H, b = L * (m + 1) / H;
-      if constexpr (b > a) __builtin_amdgcn_sched_group_barrier(0x020, b - a, 0);  // global loads
-    } else {
-      constexpr int a = Wn * (m - H) / H, b = Wn * (m - H + 1) / H;
-      if constexpr (b > a) __builtin_amdgcn_sched_group_barrier(0x200, b - a, 0);  // LDS stores
-    }
-    sched_mfma_seq<m + 1, S, P, F, L, Wn>();
-  }
-}
-template <int S, int P, int F, int L, int Wn>
-__device__ __forceinline__ void sched_kblock() {
-  __builtin_amdgcn_sched_group_barrier(0x100, F, 0);  // step 0's fragment reads
-  sched_mfma_seq<0, S, P, F, L, Wn>();
+// Workgroup barrier that also fences the compiler: no instruction is moved
+// across it, and memory accesses stay on their side (the hardware waits are
+// the explicit s_waitcnt above).
+__device__ __forceinline__ void phase_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_barrier" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int BM, int BN, int WM, int WN, bool GATED>
-__global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(1, 1))) void tiled_kernel(
-    GemmArgs a) {
-  constexpr int kThreads = WM * WN * kWave;
-  constexpr int WTM = BM / WM, WTN = BN / WN;
-  constexpr int TM = WTM / 32, TN = WTN / 32;
-  constexpr int X_CH = BM * 8 / kThreads;
-  constexpr int W_CH = BN * 8 / kThreads;
-  constexpr int RSTRIDE = kThreads / 8;  // rows between a thread's consecutive chunks
-  constexpr int kXBytes = BM * 128;
-  constexpr int kBufBytes = (BM + BN) * 128;
-  constexpr int OUT_COLS = GATED ? BN / 2 : BN;
-  static_assert(TM >= 1 && TN >= 1 && (!GATED || TN % 2 == 0), "tile shape");
-  static_assert(X_CH * kThreads == BM * 8 && W_CH * kThreads == BN * 8, "chunking");
-  static_assert(RSTRIDE % 16 == 0, "swizzle key repeats every 16 rows");
+// 64 lanes x 16 bytes from rsrc + voff[lane] to lds + 16 * lane.
+__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t rs, unsigned char* lds, uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)lds, 16, voff, 0, 0, 0);
+}
+
+template <bool GATED>
+__global__ __launch_bounds__(kThreads) void tiled_kernel(GemmArgs a) {
+  constexpr int OUT_COLS = GATED ? kBN / 2 : kBN;
+  constexpr uint32_t kInvalid = 0x80000000u;
+  constexpr int kRecords = 0x7fffffff;
+  constexpr int kRsrcWord3 = 0x00020000;
 
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  __shared__ int mt_prefix[kMaxGroups + 1];
+  __shared__ int mt_prefix[kMaxGroups + 1];  // first m-tile of each group
+  __shared__ int row_off[kMaxGroups + 1];    // the group offsets, read once
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
-  const int wave = tid / kWave;
-  const int wm = wave % WM, wn = wave / WM;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int grp = wave >> 2, q = wave & 3;
   const int lrow = lane & 31, lhalf = lane >> 5;
   const int n_tiles_n = ceil_div(a.N, OUT_COLS);
 
   int total_mt;
   if (a.offsets == nullptr) {
-    total_mt = ceil_div(a.static_rows, BM);
+    total_mt = ceil_div(a.static_rows, kBM);
   } else {
     if (wave == 0) {
       int carry = 0;
       for (int g0 = 0; g0 < a.groups; g0 += kWave) {
         const int g = g0 + lane;
-        const int cnt = g < a.groups ? ceil_div(a.offsets[g + 1] - a.offsets[g], BM) : 0;
+        int cnt = 0;
+        if (g < a.groups) {
+          const int lo = a.offsets[g], hi = a.offsets[g + 1];
+          row_off[g] = lo;
+          if (g + 1 == a.groups) row_off[g + 1] = hi;
+          cnt = ceil_div(hi - lo, kBM);
+        }
         int inc = cnt;
 #pragma unroll
         for (int off = 1; off < kWave; off <<= 1) {
@@ -123,40 +131,40 @@ __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(1
 
   // XCD-aware renumbering (gridDim.x is a multiple of 8)
   const int per_xcd = gridDim.x / 8;
-  int tile = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  if (tile >= total_tiles) return;
-
-  const int cc = tid & 7;   // 16-byte chunk of a 128-byte K-block row
-  const int r0 = tid >> 3;  // first row this thread stages
-  const int x_lds0 = r0 * 128 + ((cc ^ swz(r0)) << 4);
-  const int w_lds0 = kXBytes + x_lds0;
-  const int frag_slot = swz(lrow);  // swizzle key of the rows a lane reads
+  const int first = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (first >= total_tiles) return;
   const int nkb = ceil_div(a.K, kBK);
-  static_assert(!GATED || (WTN / 2) % RSTRIDE == 0, "gate/up half of a chunk is static");
+  const int n_stages = ceil_div(total_tiles - first, gridDim.x) * nkb;
 
   struct TileInfo {
     int g, row_base, m, m0, nt;
   };
+  // Tile order: group, then n-tile, then m-tile (fastest).  The m-tiles of a
+  // group that share one weight tile are neighbours, so they run at the same
+  // time on one XCD and the weights cross the fabric once.
   auto tile_info = [&](int t) {
     TileInfo ti;
-    const int mt = t / n_tiles_n;
-    ti.nt = t - mt * n_tiles_n;
+    int mg = total_mt, base = 0;  // m-tiles of the group, first tile id of the group
     ti.g = 0;
     ti.row_base = 0;
     ti.m = a.static_rows;
-    ti.m0 = mt * BM;
     if (a.offsets != nullptr) {
       int lo = 0, hi = a.groups - 1;
       while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
-        if (mt_prefix[mid] <= mt) lo = mid; else hi = mid - 1;
+        if (mt_prefix[mid] * n_tiles_n <= t) lo = mid; else hi = mid - 1;
       }
+      // from LDS: a global load here would make the compiler wait for every
+      // stage load in flight (they share the vector memory counter)
       ti.g = lo;
-      ti.row_base = a.offsets[lo];
-      ti.m = a.offsets[lo + 1] - ti.row_base;
-      ti.m0 = (mt - mt_prefix[lo]) * BM;
+      ti.row_base = row_off[lo];
+      ti.m = row_off[lo + 1] - ti.row_base;
+      base = mt_prefix[lo] * n_tiles_n;
+      mg = mt_prefix[lo + 1] - mt_prefix[lo];
     }
-    // every field is the same across the workgroup; keep it in scalar registers
+    const int local = t - base;
+    ti.nt = local / mg;
+    ti.m0 = (local - ti.nt * mg) * kBM;
     ti.g = __builtin_amdgcn_readfirstlane(ti.g);
     ti.row_base = __builtin_amdgcn_readfirstlane(ti.row_base);
     ti.m = __builtin_amdgcn_readfirstlane(ti.m);
@@ -165,152 +173,132 @@ __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(1
     return ti;
   };
 
-  // Buffer loads: the tile's bases live in scalar resource descriptors and
-  // each staged chunk keeps one 32-bit byte offset.  Offsets >= 2^31 lie past
-  // num_records, so rows past the group, columns past N and the K tail read
-  // as zeros without touching memory.
-  constexpr uint32_t kInvalid = 0x80000000u;
-  constexpr int kRecords = 0x7fffffff;
-  constexpr int kRsrcWord3 = 0x00020000;
-  __amdgpu_buffer_rsrc_t rs_x, rs_w0, rs_w1;
-  uint32_t xoff[X_CH], woff[W_CH];
-  auto setup = [&](const TileInfo& ti) {
-    rs_x = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint16_t*>(a.x + static_cast<size_t>(ti.row_base + ti.m0) * a.K), 0, kRecords, kRsrcWord3);
-    const size_t wg = static_cast<size_t>(ti.g) * a.group_stride;
-    const int col0 = ti.nt * OUT_COLS;
-    rs_w0 = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.w0 + wg + static_cast<size_t>(col0) * a.ldw),
-                                              0, kRecords, kRsrcWord3);
-    rs_w1 = rs_w0;
-    if constexpr (GATED)
-      rs_w1 = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.w1 + wg + static_cast<size_t>(col0) * a.ldw),
-                                                0, kRecords, kRsrcWord3);
-#pragma unroll
-    for (int i = 0; i < X_CH; ++i) {
-      const int r = r0 + i * RSTRIDE;
-      xoff[i] = (ti.m0 + r < ti.m) ? static_cast<uint32_t>(r * a.K * 2 + cc * 16) : kInvalid;
+  // ---- load side: runs three stages ahead of the compute side ----
+  // Group 0 fills the X part of every stage and group 1 the W part, each in
+  // its own memory phase, so no wave issues loads between its MFMAs.  Wave q
+  // of a group fills the 16-row blocks 4q..4q+3 of its part.  A lane's LDS
+  // slot is lane & 3 of row lane >> 2 of a block, so the global chunk it
+  // fetches, (lane & 3) ^ ((row >> 2) & 3), depends on the lane only.
+  const int chunk = (lane & 3) ^ ((lane >> 4) & 3);
+  __amdgpu_buffer_rsrc_t rs_ld;  // X (group 0) or W (group 1) of the tile being loaded
+  u32x4 ld_off;                  // byte offset of each load's row, or >= 2^31
+  int ld_tile = first, ld_kb = 0;
+  auto ld_setup = [&](int t) {
+    if (t >= total_tiles) {  // past this workgroup's last tile: empty loads keep the count regular
+      ld_off = u32x4{kInvalid, kInvalid, kInvalid, kInvalid};
+      return;
     }
+    const TileInfo ti = tile_info(t);
+    if (grp == 0) {
+      rs_ld = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<uint16_t*>(a.x + static_cast<size_t>(ti.row_base + ti.m0) * a.K), 0, kRecords, kRsrcWord3);
 #pragma unroll
-    for (int i = 0; i < W_CH; ++i) {
-      const int n = r0 + i * RSTRIDE;
-      int lcol;  // column relative to col0
-      if constexpr (GATED) {
-        const int wn_ = n / WTN, within = n % WTN;
-        lcol = wn_ * (WTN / 2) + within % (WTN / 2);
-      } else {
-        lcol = n;
+      for (int i = 0; i < 4; ++i) {
+        const int r = 16 * (4 * q + i) + (lane >> 2);  // token row within the tile
+        ld_off[i] = (ti.m0 + r < ti.m) ? static_cast<uint32_t>(r * a.K * 2 + chunk * 16) : kInvalid;
       }
-      woff[i] = (col0 + lcol < a.N) ? static_cast<uint32_t>(lcol * a.ldw * 2) : kInvalid;
+    } else {
+      const int col0 = ti.nt * OUT_COLS;
+      // the wave's 64 weight rows 64q..64q+63 are all gate rows or all up rows
+      const bool up = GATED && (q & 1);
+      const uint16_t* wbase = (up ? a.w1 : a.w0) + static_cast<size_t>(ti.g) * a.group_stride +
+                              static_cast<size_t>(col0) * a.ldw;
+      rs_ld = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(wbase), 0, kRecords, kRsrcWord3);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = 16 * (4 * q + i) + (lane >> 2);            // weight row within the tile
+        const int lcol = GATED ? (r >> 7) * 64 + (r & 63) : r;  // output column relative to col0
+        ld_off[i] = (col0 + lcol < a.N) ? static_cast<uint32_t>(lcol * a.ldw * 2 + chunk * 16) : kInvalid;
+      }
     }
   };
-
-  // staging registers: the next K-block is in flight while this one feeds the MFMAs
-  u32x4 sx0[X_CH], sw0[W_CH];
-  auto load_block = [&](int kb, u32x4 (&rx)[X_CH], u32x4 (&rw)[W_CH]) {
-    // K offsets are added to the per-chunk offsets (each below 2^31, so the
-    // sum cannot wrap) and the K-tail mark is or-ed in afterwards
-    const int kk = kb * kBK + cc * 8;
-    const uint32_t kmask = (kb < nkb && kk < a.K) ? 0u : kInvalid;  // past the end: no traffic
-    const uint32_t wk = static_cast<uint32_t>((kk < a.K ? weight_col_offset(a, kk) : 0) * 2);
-    const uint32_t xk = static_cast<uint32_t>(kb * kBK * 2);
-#pragma unroll
-    for (int i = 0; i < X_CH; ++i)
-      rx[i] = __builtin_amdgcn_raw_buffer_load_b128(rs_x, (xoff[i] + xk) | kmask, 0, 0);
-#pragma unroll
-    for (int i = 0; i < W_CH; ++i) {
-      // a chunk row r0 + i*RSTRIDE lies in the up half iff i*RSTRIDE does (r0 < RSTRIDE)
-      const bool up_half = GATED && ((i * RSTRIDE) % WTN) >= WTN / 2;
-      rw[i] = __builtin_amdgcn_raw_buffer_load_b128(up_half ? rs_w1 : rs_w0, (woff[i] + wk) | kmask, 0, 0);
+  // Byte offset of the stage's K origin (added to every load's row-and-chunk
+  // offset) and the mark of a chunk past K.  The offset is the same for all
+  // lanes except for weights whose K range is stacked from segments that a
+  // 32-wide stage can straddle.
+  uint32_t ld_k = 0, ld_kmask = 0;
+  auto ld_kstep = [&]() {
+    const int k0 = ld_kb * kBK;
+    ld_kmask = k0 + chunk * 8 < a.K ? 0u : kInvalid;
+    if (grp == 0 || a.kseg >= a.K) {
+      ld_k = static_cast<uint32_t>(k0 * 2);
+    } else if (a.kseg % kBK == 0) {
+      const int seg = k0 / a.kseg;
+      ld_k = static_cast<uint32_t>((static_cast<size_t>(seg) * a.seg_stride + (k0 - seg * a.kseg)) * 2);
+    } else {
+      const int kk = min(k0 + chunk * 8, a.K - 8);
+      ld_k = static_cast<uint32_t>((weight_col_offset(a, kk) - static_cast<size_t>(kk - k0)) * 2);
     }
   };
-  auto store_block = [&](int buf, const u32x4 (&rx)[X_CH], const u32x4 (&rw)[W_CH]) {
-    unsigned char* b = smem + buf * kBufBytes;
+  // load i (of 4) of this wave's part of the stage being loaded, into buffer buf
+  auto load_one = [&](int buf, int i) {
+    load_lds16(rs_ld, smem + buf * kStageBytes + grp * kPartBytes + q * 4096 + i * 1024,
+               (ld_off[i] + ld_k) | ld_kmask);
+  };
+  auto ld_advance = [&]() {  // after the four loads of a stage
+    if (++ld_kb == nkb) {
+      ld_kb = 0;
+      ld_tile += gridDim.x;
+      ld_setup(ld_tile);
+    }
+    ld_kstep();
+  };
+  auto issue = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < X_CH; ++i) *reinterpret_cast<u32x4*>(b + x_lds0 + i * RSTRIDE * 128) = rx[i];
-#pragma unroll
-    for (int i = 0; i < W_CH; ++i) *reinterpret_cast<u32x4*>(b + w_lds0 + i * RSTRIDE * 128) = rw[i];
+    for (int i = 0; i < 4; ++i) load_one(buf, i);
+    ld_advance();
   };
 
-  TileInfo cur = tile_info(tile);
-  setup(cur);
-  load_block(0, sx0, sw0);
-  f32x16 acc[TN][TM];
-
-  auto compute = [&](int buf) {
-    const unsigned char* b = smem + buf * kBufBytes;
-    // fragments double-buffered across the four 16-wide K-steps: the reads
-    // of step s+1 are in flight while step s's MFMAs issue
-    bf16x8 wf[2][TN], xf[2][TM];
-    auto read_frags = [&](int ks, bf16x8 (&w)[TN], bf16x8 (&x)[TM]) {
-      const int slot = ((2 * ks + lhalf) ^ frag_slot) << 4;
+  // ---- compute side ----
+  const int xrow0 = grp * 128 + (q & 1) * 64;  // this wave's token rows in the tile
+  const int wrow0 = (q >> 1) * 128;            // and its weight rows
+  const int rsw = (lrow >> 2) & 3;             // slot key of the rows this lane reads
+  bf16x8 xf[2][2], wf[2][4];                   // [k-step][tile]
+  f32x16 acc[4][2];
+  auto read_frags = [&](int buf, int ks) {  // the fragments of one K-step
+    const unsigned char* b = smem + buf * kStageBytes;
+    {
+      const int slot = ((2 * ks + lhalf) ^ rsw) << 4;
 #pragma unroll
-      for (int tn = 0; tn < TN; ++tn)
-        w[tn] = as_bf16x8(*reinterpret_cast<const u32x4*>(b + kXBytes + (wn * WTN + tn * 32 + lrow) * 128 + slot));
+      for (int tn = 0; tn < 4; ++tn)
+        wf[ks][tn] = as_bf16x8(*reinterpret_cast<const u32x4*>(b + kPartBytes + (wrow0 + tn * 32 + lrow) * kRowBytes + slot));
 #pragma unroll
-      for (int tm = 0; tm < TM; ++tm)
-        x[tm] = as_bf16x8(*reinterpret_cast<const u32x4*>(b + (wm * WTM + tm * 32 + lrow) * 128 + slot));
-    };
-    read_frags(0, wf[0], xf[0]);
-#pragma unroll
-    for (int ks = 0; ks < kBK / 16; ++ks) {
-      if (ks + 1 < kBK / 16) read_frags(ks + 1, wf[(ks + 1) & 1], xf[(ks + 1) & 1]);
-#pragma unroll
-      for (int tn = 0; tn < TN; ++tn)
-#pragma unroll
-        for (int tm = 0; tm < TM; ++tm)
-          acc[tn][tm] = mfma32x32x16(wf[ks & 1][tn], xf[ks & 1][tm], acc[tn][tm]);
+      for (int tm = 0; tm < 2; ++tm)
+        xf[ks][tm] = as_bf16x8(*reinterpret_cast<const u32x4*>(b + (xrow0 + tm * 32 + lrow) * kRowBytes + slot));
     }
   };
-  // One K-block, a single basic block so the scheduler can interleave it:
-  // load block kb+1 into registers, multiply block kb from LDS, store kb+1
-  // into the other LDS buffer (past the last block the loads are masked and
-  // the store lands in the idle buffer).
-  auto kblock = [&](int kb) {
-    load_block(kb + 1, sx0, sw0);
-    compute(kb & 1);
-    store_block((kb + 1) & 1, sx0, sw0);
-    sched_kblock<kBK / 16, TM * TN, TM + TN, X_CH + W_CH, X_CH + W_CH>();
-    __syncthreads();
+  auto mfma_step = [&](int ks) {
+#pragma unroll
+    for (int tn = 0; tn < 4; ++tn)
+#pragma unroll
+      for (int tm = 0; tm < 2; ++tm) acc[tn][tm] = mfma32x32x16(wf[ks][tn], xf[ks][tm], acc[tn][tm]);
   };
-
-  while (true) {
-    store_block(0, sx0, sw0);
-    __syncthreads();
+  auto zero_acc = [&]() {
 #pragma unroll
-    for (int tn = 0; tn < TN; ++tn)
+    for (int tn = 0; tn < 4; ++tn)
 #pragma unroll
-      for (int tm = 0; tm < TM; ++tm) acc[tn][tm] = f32x16{};
-    for (int kb = 0; kb < nkb; ++kb) kblock(kb);
-
-    // start the next tile's first K-block before this tile's epilogue
-    const int next = tile + gridDim.x;
-    TileInfo nxt{};
-    if (next < total_tiles) {
-      nxt = tile_info(next);
-      setup(nxt);
-      load_block(0, sx0, sw0);
-    }
-
-    // epilogue: lane holds C[n = 8*(v/4) + 4*lhalf + v%4][t = lrow] per 32x32 tile
+      for (int tm = 0; tm < 2; ++tm) acc[tn][tm] = f32x16{};
+  };
+  // lane holds C[n = 8*(v/4) + 4*lhalf + v%4][t = lrow] of each 32x32 tile
+  auto epilogue = [&](const TileInfo& ti) {
 #pragma unroll
-    for (int tm = 0; tm < TM; ++tm) {
-      const int row = cur.m0 + wm * WTM + tm * 32 + lrow;
-      if (row >= cur.m) continue;
-      uint16_t* orow = a.out + static_cast<size_t>(cur.row_base + row) * a.N;
-      constexpr int TOUT = GATED ? TN / 2 : TN;
+    for (int tm = 0; tm < 2; ++tm) {
+      const int row = ti.m0 + xrow0 + tm * 32 + lrow;
+      if (row >= ti.m) continue;
+      uint16_t* orow = a.out + static_cast<size_t>(ti.row_base + row) * a.N;
+      constexpr int TOUT = GATED ? 2 : 4;
 #pragma unroll
       for (int tn = 0; tn < TOUT; ++tn) {
 #pragma unroll
         for (int v4 = 0; v4 < 4; ++v4) {
-          const int col = GATED ? cur.nt * OUT_COLS + wn * (WTN / 2) + tn * 32 + 8 * v4 + 4 * lhalf
-                                : cur.nt * BN + wn * WTN + tn * 32 + 8 * v4 + 4 * lhalf;
+          const int col = ti.nt * OUT_COLS + (q >> 1) * (GATED ? 64 : 128) + tn * 32 + 8 * v4 + 4 * lhalf;
           if (col >= a.N) continue;
           float o[4];
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const float c0 = acc[tn][tm][4 * v4 + i];
             if constexpr (GATED)
-              o[i] = silu(c0) * acc[tn + TN / 2][tm][4 * v4 + i];
+              o[i] = silu(c0) * acc[tn + 2][tm][4 * v4 + i];
             else
               o[i] = c0;
           }
@@ -321,10 +309,61 @@ __global__ __launch_bounds__(WM* WN* kWave) __attribute__((amdgpu_waves_per_eu(1
         }
       }
     }
-    if (next >= total_tiles) break;
-    tile = next;
-    cur = nxt;
+  };
+
+  // ---- pipeline ----
+  TileInfo cur = tile_info(first);
+  int cur_tile = first, kb = 0;
+  zero_acc();
+  ld_setup(first);
+  ld_kstep();
+  issue(0);
+  issue(1);
+  issue(2);
+  __builtin_amdgcn_s_waitcnt(wait_vm(2 * kLoadsPerStage));  // own stage-0 loads landed
+  phase_barrier();
+  if (grp == 1) phase_barrier();  // group 1 runs one phase behind
+  for (int j = 0; j < n_stages; ++j) {
+    // memory phase of stage j
+    if (kb == 0 && j > 0) {
+      epilogue(cur);
+      zero_acc();
+      cur_tile += gridDim.x;
+      cur = tile_info(cur_tile);
+    }
+    // The stage's four loads are spread over both phases, between the LDS
+    // reads and between the MFMAs: the texture unit takes them one by one
+    // and no wave stalls on a burst of loads.
+    const int lb = (j + 3) & 3;
+    load_one(lb, 0);
+    read_frags(j & 3, 0);
+    load_one(lb, 1);
+    read_frags(j & 3, 1);
+    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+    if (grp == 1) __builtin_amdgcn_s_waitcnt(wait_vm(kLoadsPerStage + 2));  // own stage j+1 landed
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    phase_barrier();
+    // compute phase of stage j
+    mfma_step(0);
+    load_one(lb, 2);
+    mfma_step(1);
+    load_one(lb, 3);
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    if (grp == 0) __builtin_amdgcn_s_waitcnt(wait_vm(2 * kLoadsPerStage));  // own stage j+1 landed
+    phase_barrier();
+    ld_advance();
+    if (++kb == nkb) kb = 0;
   }
+  if (grp == 0) phase_barrier();  // matches group 1's extra barrier
+  epilogue(cur);
+  __builtin_amdgcn_s_waitcnt(kWaitAll);  // no load may land in LDS after the workgroup ends
 }
 
 int device_cu_count() {
@@ -340,29 +379,23 @@ int device_cu_count() {
   return cus;
 }
 
-template <int BM, int BN, int WM, int WN, bool GATED>
+template <bool GATED>
 hipError_t launch_tiled_t(const Segments& seg, const GemmArgs& a, hipStream_t st) {
-  constexpr int kThreads = WM * WN * kWave;
-  constexpr int OUT_COLS = GATED ? BN / 2 : BN;
-  constexpr size_t kLds = 2 * (BM + BN) * 128;
-  constexpr int kWgsPerCu = static_cast<int>((160 * 1024) / (kLds + 8 * 1024)) > 0
-                                ? static_cast<int>((160 * 1024) / (kLds + 8 * 1024))
-                                : 1;
+  constexpr int OUT_COLS = GATED ? kBN / 2 : kBN;
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&tiled_kernel<BM, BN, WM, WN, GATED>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kLds));
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&tiled_kernel<GATED>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  const long long m_tiles = (a.offsets ? static_cast<long long>(ceil_div(seg.total_rows, BM)) + seg.groups
-                                       : ceil_div(seg.static_rows, BM));
+  const long long m_tiles = (a.offsets ? static_cast<long long>(ceil_div(seg.total_rows, kBM)) + seg.groups
+                                       : ceil_div(seg.static_rows, kBM));
   const long long tiles = m_tiles * ceil_div(a.N, OUT_COLS);
   if (tiles == 0) return hipSuccess;
-  long long grid = std::min<long long>(tiles, static_cast<long long>(device_cu_count()) * kWgsPerCu);
+  long long grid = std::min<long long>(tiles, device_cu_count());  // one workgroup per CU (LDS)
   grid = ((grid + 7) / 8) * 8;
-  hipLaunchKernelGGL((tiled_kernel<BM, BN, WM, WN, GATED>), dim3(static_cast<unsigned>(grid)),
-                     dim3(kThreads), kLds, st, a);
+  hipLaunchKernelGGL((tiled_kernel<GATED>), dim3(static_cast<unsigned>(grid)), dim3(kThreads), kLdsBytes, st, a);
   return hipGetLastError();
 }
 
@@ -370,8 +403,12 @@ hipError_t launch_tiled_t(const Segments& seg, const GemmArgs& a, hipStream_t st
 
 hipError_t launch_tiled(const Segments& seg, const GemmArgs& a, bool gated, hipStream_t st) {
   if (seg.groups > kMaxGroups) return hipErrorInvalidValue;
-  return gated ? launch_tiled_t<256, 256, 4, 2, true>(seg, a, st)
-               : launch_tiled_t<256, 256, 4, 2, false>(seg, a, st);
+  // 32-bit byte offsets: a tile's X rows and a group's weight columns
+  const size_t x_span = static_cast<size_t>(kBM) * a.K * 2;
+  const size_t w_span = (static_cast<size_t>(kBN) * a.ldw +
+                         (a.kseg < a.K ? static_cast<size_t>((a.K - 1) / a.kseg) * a.seg_stride : 0) + a.K) * 2;
+  if (x_span >= 0x80000000ull || w_span >= 0x80000000ull) return hipErrorInvalidValue;
+  return gated ? launch_tiled_t<true>(seg, a, st) : launch_tiled_t<false>(seg, a, st);
 }
 
 hipError_t launch_ffn_up(const Segments& seg, const UpArgs& u, hipStream_t st) {
