@@ -1,9 +1,11 @@
 // Weighted combine back to token order (Sec. 2.1: expert outputs are
 // combined and returned):
 //   out[t] = sum_{j<k, inv_pos[t*k+j] >= 0} w[t][j] * y_perm[inv_pos[t*k+j]] + y_shared[t]
-// One wave per token; each lane owns 16-byte column vectors of the row and
-// accumulates in fp32, j ascending then the shared term, so the result does
-// not depend on scheduling.  Bandwidth-bound: every byte is read once.
+// One wave per (token, 64 consecutive 16-byte column vectors of its row), so
+// that even a decode-sized batch spreads over the whole chip; each lane owns
+// one vector and accumulates in fp32, j ascending then the shared term, so
+// the result does not depend on scheduling.  Bandwidth-bound: every byte of
+// y_perm and y_shared is read once.
 #include "common.h"
 #include "kernels.h"
 
@@ -19,19 +21,24 @@ __global__ __launch_bounds__(256) void combine_kernel(int T, int k, int H,
                                                       const uint16_t* __restrict__ y_shared,
                                                       uint16_t* __restrict__ out) {
   const int lane = lane_id();
-  const int n_waves = gridDim.x * (blockDim.x / kWave);
+  const long long n_waves = static_cast<long long>(gridDim.x) * (blockDim.x / kWave);
   const int vpr = H / 8;
-  for (int t = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave; t < T; t += n_waves) {
-    // the token's k (row, weight) pairs, gathered once per wave
+  const int chunks = ceil_div(vpr, kWave);
+  const long long n_items = static_cast<long long>(T) * chunks;
+  for (long long item = static_cast<long long>(blockIdx.x) * (blockDim.x / kWave) + threadIdx.x / kWave;
+       item < n_items; item += n_waves) {
+    const int t = static_cast<int>(item / chunks);
+    const int v0 = static_cast<int>(item - static_cast<long long>(t) * chunks) * kWave;
+    // the token's k (row, weight) pairs
     int pos = -1;
     float w = 0.0f;
     if (lane < k) {
       pos = inv_pos[static_cast<size_t>(t) * k + lane];
       w = topk_w[static_cast<size_t>(t) * k + lane];
     }
-    // the whole wave walks the row in lock-step so every lane takes part in
-    // the shuffles; lanes past the end of the row only skip the memory work
-    for (int v0 = 0; v0 < vpr; v0 += kWave) {
+    // every lane takes part in the shuffles; lanes past the end of the row
+    // only skip the memory work
+    {
       const int v = v0 + lane;
       const bool active = v < vpr;
       float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -71,7 +78,8 @@ hipError_t launch_combine(int T, int k, int H, const uint16_t* y_perm, const int
   if (T == 0) return hipSuccess;
   if (k > kMaxK) return hipErrorInvalidValue;
   const int waves_per_block = 4;
-  const int blocks = min(ceil_div(T, waves_per_block), 8192);
+  const long long items = static_cast<long long>(T) * ceil_div(H / 8, kWave);
+  const int blocks = static_cast<int>(std::min<long long>((items + waves_per_block - 1) / waves_per_block, 8192));
   hipLaunchKernelGGL(combine_kernel, dim3(blocks), dim3(waves_per_block * kWave), 0, st, T, k, H,
                      y_perm, inv_pos, topk_w, y_shared, out);
   return hipGetLastError();

@@ -11,9 +11,12 @@ namespace moe {
 // col_offset(c) = c for a single K segment (kseg >= K) or
 // (c / kseg)*seg_stride + c % kseg for K stacked over several experts.
 // GATED kernels read two such matrices (w0 = gate, w1 = up) and write
-// silu(gate) * up.  x rows have stride K and out rows stride N.
+// silu(gate) * up.  x rows have stride K and out rows stride N; row r of the
+// grouped activation matrix is x[x_rows[r]] when x_rows != nullptr
+// (weight-streaming kernel only).
 struct GemmArgs {
   const uint16_t* x;
+  const int32_t* x_rows;
   const int32_t* offsets;  // [groups+1] device, or nullptr for one group of static_rows
   int static_rows;
   int groups;

@@ -79,7 +79,8 @@ __global__ __launch_bounds__(NMAT* KP* kWave) void skinny_kernel(GemmArgs a) {
     for (int c = 0; c < 2; ++c) {
       const int tok = tok0 + c * 32 + (lane & 31);
       tok_ok[c] = c < nch && tok < m;
-      xrow[c] = a.x + static_cast<size_t>(row_base + (tok_ok[c] ? tok : 0)) * a.K + 8 * (lane >> 5);
+      const int r = row_base + (tok_ok[c] ? tok : 0);
+      xrow[c] = a.x + static_cast<size_t>(a.x_rows ? a.x_rows[r] : r) * a.K + 8 * (lane >> 5);
     }
 
     u32x4 st[DEPTH][CPL];

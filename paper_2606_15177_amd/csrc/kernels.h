@@ -45,16 +45,22 @@ struct Segments {
   int total_rows;
 };
 
-// h[r][i] = silu(sum_c x[r][c] Wg[g][i][c]) * (sum_c x[r][c] Wu[g][i][c]),
+// h[r][i] = silu(sum_c X[r][c] Wg[g][i][c]) * (sum_c X[r][c] Wu[g][i][c]),
 // weights [groups][N][K] (group stride N*K), x row stride K, h row stride N.
+// X[r] = x[r], or x[x_rows[r]] when x_rows != nullptr (the dispatch gather
+// read in place); x_rows is accepted only when ffn_up_reads_rows(seg).
 struct UpArgs {
   const uint16_t* x;
   const uint16_t* w_gate;
   const uint16_t* w_up;
   uint16_t* h;
   int K, N;
+  const int32_t* x_rows;
 };
 hipError_t launch_ffn_up(const Segments& seg, const UpArgs& a, hipStream_t st);
+// True when the gate/up GEMM for these segments can read its rows through an
+// index (the weight-streaming kernel for decode-sized groups).
+bool ffn_up_reads_rows(const Segments& seg);
 
 // y[r][n] = sum_c h[r][c] Wd(g, n, c), h row stride K, y row stride N.
 // Wd(g, n, c) = w[g*group_stride + (c / kseg)*seg_stride + n*ldw + c % kseg]

@@ -122,7 +122,7 @@ int weights_ok(const moe_dims* d, const moe_weights* w) {
 }
 
 // The two grouped GEMMs of the experts (routed, then shared) + their events.
-int run_ffn(const moe_dims* d, const uint16_t* x_perm, const int32_t* offsets,
+int run_ffn(const moe_dims* d, const uint16_t* x_perm, const int32_t* x_rows, const int32_t* offsets,
             const moe_weights* w, const uint16_t* x, uint16_t* y_perm, uint16_t* y_shared,
             void* ws, const moe_taps* taps, hipStream_t st) {
   const size_t rows = static_cast<size_t>(d->T) * d->k;
@@ -135,10 +135,10 @@ int run_ffn(const moe_dims* d, const uint16_t* x_perm, const int32_t* offsets,
   hipError_t e;
 
   record(taps, 2 * MOE_STAGE_FFN_UP, st);
-  e = moe::launch_ffn_up(routed, moe::UpArgs{x_perm, w->w_gate, w->w_up, h, d->H, d->I}, st);
+  e = moe::launch_ffn_up(routed, moe::UpArgs{x_perm, w->w_gate, w->w_up, h, d->H, d->I, x_rows}, st);
   if (e != hipSuccess) return MOE_ERR_DEVICE;
   if (d->n_shared > 0) {
-    e = moe::launch_ffn_up(shared, moe::UpArgs{x, w->sh_gate, w->sh_up, h_sh, d->H, shw}, st);
+    e = moe::launch_ffn_up(shared, moe::UpArgs{x, w->sh_gate, w->sh_up, h_sh, d->H, shw, nullptr}, st);
     if (e != hipSuccess) return MOE_ERR_DEVICE;
   }
   record(taps, 2 * MOE_STAGE_FFN_UP + 1, st);
@@ -246,7 +246,7 @@ int moe_expert_ffn(const moe_dims* d, const moe_bf16* x_perm, const int32_t* off
   s = check_ws(d, MOE_ENTRY_EXPERT_FFN, ws, ws_bytes);
   if (s != MOE_OK) return s;
   if (d->T == 0) return MOE_OK;
-  return run_ffn(d, x_perm, offsets, w, x, y_perm, y_shared, ws, nullptr,
+  return run_ffn(d, x_perm, nullptr, offsets, w, x, y_perm, y_shared, ws, nullptr,
                  static_cast<hipStream_t>(stream));
 }
 
@@ -299,12 +299,19 @@ int moe_forward(const moe_dims* d, const float* logits, const int32_t* src, cons
   e = moe::launch_permute(d->T, d->k, d->E, d->E_local, local_experts, topk_idx, offsets,
                           perm_token, inv_pos, fw.permute_ws, st);
   if (e != hipSuccess) return MOE_ERR_DEVICE;
-  e = moe::launch_gather_rows(d->T * d->k, d->H, perm_token, offsets + d->E_local, x, fw.x_perm, st);
-  if (e != hipSuccess) return MOE_ERR_DEVICE;
+  // decode-sized groups: the gate/up kernel reads x through perm_token
+  // instead of a gathered copy
+  const moe::Segments routed_seg{offsets, d->E_local, 0, d->T, d->T * d->k};
+  const bool direct = moe::ffn_up_reads_rows(routed_seg);
+  if (!direct) {
+    e = moe::launch_gather_rows(d->T * d->k, d->H, perm_token, offsets + d->E_local, x, fw.x_perm, st);
+    if (e != hipSuccess) return MOE_ERR_DEVICE;
+  }
   record(taps, 2 * MOE_STAGE_PERMUTE + 1, st);
 
   if (d->T > 0) {
-    s = run_ffn(d, fw.x_perm, offsets, w, x, fw.y_perm, fw.y_shared, fw.ffn_ws, taps, st);
+    s = run_ffn(d, direct ? x : fw.x_perm, direct ? perm_token : nullptr, offsets, w, x, fw.y_perm,
+                fw.y_shared, fw.ffn_ws, taps, st);
     if (s != MOE_OK) return s;
   } else {
     record(taps, 2 * MOE_STAGE_FFN_UP, st);

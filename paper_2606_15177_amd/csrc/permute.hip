@@ -10,8 +10,9 @@
 //              pairs of one slot inside a 64-pair chunk are ranked with a
 //              ballot + popcount, so ties keep token order without depending
 //              on atomic order.  Writes perm_token and inv_pos.
-// The row gather x_perm[r] = x[perm_token[r]] is a fourth, bandwidth-bound
-// kernel that copies 16-byte vectors.
+// When all pairs fit in one tile (decode-sized batches) a single one-block
+// kernel does the three steps.  The row gather x_perm[r] = x[perm_token[r]]
+// is a separate, bandwidth-bound kernel that copies 16-byte vectors.
 #include "common.h"
 #include "kernels.h"
 
@@ -43,6 +44,34 @@ __device__ void build_slot_map(int* slot_of, int E, int E_local, const int32_t* 
 
 __device__ __forceinline__ int slot_lookup(const int* slot_of, int e, int E) {
   return (e >= 0 && e < E) ? slot_of[e] : -1;
+}
+
+// Pairs of one slot inside a 64-pair chunk, ranked by ballot + popcount
+__device__ __forceinline__ void scatter_chunk(int p, int n_pairs, int k, int E, const int* slot_of,
+                                              int* next, const int32_t* __restrict__ topk_idx,
+                                              int32_t* __restrict__ perm_token,
+                                              int32_t* __restrict__ inv_pos) {
+  const int lane = lane_id();
+  const uint64_t below = (1ull << lane) - 1ull;
+  int s = -1;
+  if (p < n_pairs) {
+    s = slot_lookup(slot_of, topk_idx[p], E);
+    if (s < 0) inv_pos[p] = -1;
+  }
+  uint64_t pending = __ballot(s >= 0);
+  while (pending) {
+    const int leader = __ffsll(static_cast<long long>(pending)) - 1;
+    const int sl = __shfl(s, leader);
+    const uint64_t same = __ballot(s == sl);
+    const int base = next[sl];
+    if (s == sl) {
+      const int pos = base + __popcll(same & below);
+      perm_token[pos] = p / k;
+      inv_pos[p] = pos;
+    }
+    if (lane == leader) next[sl] = base + __popcll(same);
+    pending &= ~same;
+  }
 }
 
 __global__ __launch_bounds__(256) void perm_count_kernel(int n_pairs, int E, int E_local,
@@ -128,30 +157,39 @@ __global__ __launch_bounds__(kWave) void perm_scatter_kernel(
   for (int s = threadIdx.x; s < E_local; s += kWave)
     next[s] = offsets[s] + tile_prefix[static_cast<size_t>(tile) * E_local + s];
   build_slot_map(slot_of, E, E_local, local_experts);
-  const int lane = lane_id();
-  const uint64_t below = (1ull << lane) - 1ull;
-  for (int c0 = tile * kTile; c0 < min(n_pairs, (tile + 1) * kTile); c0 += kWave) {
-    const int p = c0 + lane;
-    int s = -1;
-    if (p < n_pairs) {
-      s = slot_lookup(slot_of, topk_idx[p], E);
-      if (s < 0) inv_pos[p] = -1;
-    }
-    uint64_t pending = __ballot(s >= 0);
-    while (pending) {
-      const int leader = __ffsll(static_cast<long long>(pending)) - 1;
-      const int sl = __shfl(s, leader);
-      const uint64_t same = __ballot(s == sl);
-      const int base = next[sl];
-      if (s == sl) {
-        const int pos = base + __popcll(same & below);
-        perm_token[pos] = p / k;
-        inv_pos[p] = pos;
-      }
-      if (lane == leader) next[sl] = base + __popcll(same);
-      pending &= ~same;
-    }
+  for (int c0 = tile * kTile; c0 < min(n_pairs, (tile + 1) * kTile); c0 += kWave)
+    scatter_chunk(c0 + lane_id(), n_pairs, k, E, slot_of, next, topk_idx, perm_token, inv_pos);
+}
+
+// All three steps for n_pairs <= kTile in one block of 1024 threads.
+__global__ __launch_bounds__(1024) void perm_single_kernel(int n_pairs, int k, int E, int E_local,
+                                                           const int32_t* __restrict__ local_experts,
+                                                           const int32_t* __restrict__ topk_idx,
+                                                           int32_t* __restrict__ offsets,
+                                                           int32_t* __restrict__ perm_token,
+                                                           int32_t* __restrict__ inv_pos) {
+  extern __shared__ int sm[];
+  int* slot_of = sm;
+  int* cnt = sm + E;  // per-slot count, then next free row
+  for (int s = threadIdx.x; s < E_local; s += blockDim.x) cnt[s] = 0;
+  build_slot_map(slot_of, E, E_local, local_experts);
+  for (int p = threadIdx.x; p < n_pairs; p += blockDim.x) {
+    const int s = slot_lookup(slot_of, topk_idx[p], E);
+    if (s >= 0) atomicAdd(&cnt[s], 1);
   }
+  __syncthreads();
+  const int own = threadIdx.x < E_local ? cnt[threadIdx.x] : 0;
+  int total;
+  const int excl = block_exclusive_scan(own, &total);
+  if (threadIdx.x < E_local) {
+    offsets[threadIdx.x] = excl;
+    cnt[threadIdx.x] = excl;
+  }
+  if (threadIdx.x == 0) offsets[E_local] = total;
+  __syncthreads();
+  if (threadIdx.x < kWave)
+    for (int c0 = 0; c0 < n_pairs; c0 += kWave)
+      scatter_chunk(c0 + threadIdx.x, n_pairs, k, E, slot_of, cnt, topk_idx, perm_token, inv_pos);
 }
 
 __global__ __launch_bounds__(256) void gather_rows_kernel(int H, const int32_t* __restrict__ perm_token,
@@ -184,6 +222,11 @@ hipError_t launch_permute(int T, int k, int E, int E_local, const int32_t* local
   const int n_tiles = ceil_div(n_pairs, kTile);
   int32_t* tile_counts = static_cast<int32_t*>(ws);
   const size_t lds = static_cast<size_t>(E + E_local) * sizeof(int);
+  if (n_tiles == 1) {
+    hipLaunchKernelGGL(perm_single_kernel, dim3(1), dim3(1024), lds, st, n_pairs, k, E, E_local,
+                       local_experts, topk_idx, offsets, perm_token, inv_pos);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(perm_count_kernel, dim3(n_tiles), dim3(256), lds, st, n_pairs, E, E_local,
                      local_experts, topk_idx, tile_counts);
   hipError_t err = hipGetLastError();
