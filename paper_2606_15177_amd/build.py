@@ -49,6 +49,19 @@ def _compile(src: str) -> str:
     return obj
 
 
+def _check_resolved(lib: str) -> None:
+    """A shared library links even when one of its own functions was never
+    emitted (the loader would only fail later); reject undefined symbols of
+    the library's namespace."""
+    r = subprocess.run(["nm", "-D", "--undefined-only", lib], capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"nm failed on {lib}:\n{r.stderr}")
+    missing = [ln.split()[-1] for ln in r.stdout.splitlines() if "_ZN3moe" in ln]
+    if missing:
+        os.remove(lib)
+        raise RuntimeError("library references undefined symbols of its own: " + ", ".join(missing))
+
+
 def build(verbose: bool = False) -> str:
     """Compile and link the library; returns its path."""
     os.makedirs(BUILD_DIR, exist_ok=True)
@@ -59,6 +72,7 @@ def build(verbose: bool = False) -> str:
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
+    _check_resolved(tmp)
     os.replace(tmp, LIB_PATH)
     if verbose:
         print(f"built {LIB_PATH}")

@@ -14,9 +14,20 @@ namespace moe {
 // silu(gate) * up.  x rows have stride K and out rows stride N; row r of the
 // grouped activation matrix is x[x_rows[r]] when x_rows != nullptr
 // (weight-streaming kernel only).
+//
+// Chunk-blocked layout (weight-streaming kernel with device offsets only, K
+// and N multiples of 16): a group's rows are cut into chunks of 32, the last
+// one padded (with zeros, since padded inputs give zero outputs), chunk j of
+// group g being global chunk sum_{g' < g} ceil(rows_g' / 32) + j.  Chunk c of
+// a matrix with C columns holds C/16 blocks of 1 KB, block s holding column
+// 16s + 8h + e of chunk row t at element 8*(32*h + t) + e: exactly the B
+// operand of one v_mfma_f32_32x32x16_bf16 (lane 32h + t, 8 values), so a
+// wave loads it as one contiguous 1 KB.  x_blocked reads x in this layout;
+// out_blocked writes out in it, padding rows included.
 struct GemmArgs {
   const uint16_t* x;
   const int32_t* x_rows;
+  bool x_blocked, out_blocked;
   const int32_t* offsets;  // [groups+1] device, or nullptr for one group of static_rows
   int static_rows;
   int groups;
@@ -34,6 +45,8 @@ __device__ __forceinline__ size_t weight_col_offset(const GemmArgs& a, int c) {
 }
 
 hipError_t launch_skinny(const Segments& seg, const GemmArgs& a, bool gated, hipStream_t st);
+constexpr int kChunkRows = kChunkRowsHost;
+constexpr int kBlockElems = 512;  // one 1 KB block of the chunk-blocked layout
 hipError_t launch_tiled(const Segments& seg, const GemmArgs& a, bool gated, hipStream_t st);
 
 // Largest per-group row count routed to the weight-streaming kernel.

@@ -402,7 +402,7 @@ hipError_t launch_tiled_t(const Segments& seg, const GemmArgs& a, hipStream_t st
 }  // namespace
 
 hipError_t launch_tiled(const Segments& seg, const GemmArgs& a, bool gated, hipStream_t st) {
-  if (seg.groups > kMaxGroups || a.x_rows != nullptr) return hipErrorInvalidValue;
+  if (seg.groups > kMaxGroups || a.x_rows != nullptr || a.x_blocked || a.out_blocked) return hipErrorInvalidValue;
   // 32-bit byte offsets: a tile's X rows and a group's weight columns
   const size_t x_span = static_cast<size_t>(kBM) * a.K * 2;
   const size_t w_span = (static_cast<size_t>(kBN) * a.ldw +
@@ -414,10 +414,11 @@ hipError_t launch_tiled(const Segments& seg, const GemmArgs& a, bool gated, hipS
 bool ffn_up_reads_rows(const Segments& seg) { return seg.max_rows <= kSkinnyMaxRows; }
 
 hipError_t launch_ffn_up(const Segments& seg, const UpArgs& u, hipStream_t st) {
-  if (u.x_rows && !ffn_up_reads_rows(seg)) return hipErrorInvalidValue;
+  if ((u.x_rows || u.h_blocked) && !ffn_up_reads_rows(seg)) return hipErrorInvalidValue;
   GemmArgs a{};
   a.x = u.x;
   a.x_rows = u.x_rows;
+  a.out_blocked = u.h_blocked;
   a.offsets = seg.offsets;
   a.static_rows = seg.static_rows;
   a.groups = seg.groups;
@@ -435,8 +436,10 @@ hipError_t launch_ffn_up(const Segments& seg, const UpArgs& u, hipStream_t st) {
 }
 
 hipError_t launch_ffn_down(const Segments& seg, const DownArgs& d, hipStream_t st) {
+  if (d.h_blocked && !ffn_up_reads_rows(seg)) return hipErrorInvalidValue;
   GemmArgs a{};
   a.x = d.h;
+  a.x_blocked = d.h_blocked;
   a.offsets = seg.offsets;
   a.static_rows = seg.static_rows;
   a.groups = seg.groups;

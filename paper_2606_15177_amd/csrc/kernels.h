@@ -56,11 +56,22 @@ struct UpArgs {
   uint16_t* h;
   int K, N;
   const int32_t* x_rows;
+  // write h in the chunk-blocked layout (decode-sized groups, see below)
+  bool h_blocked;
 };
 hipError_t launch_ffn_up(const Segments& seg, const UpArgs& a, hipStream_t st);
 // True when the gate/up GEMM for these segments can read its rows through an
 // index (the weight-streaming kernel for decode-sized groups).
 bool ffn_up_reads_rows(const Segments& seg);
+
+// For decode-sized groups (ffn_up_reads_rows) the gate/up GEMM may write h
+// chunk-blocked: each group's rows cut into chunks of 32 (the last one
+// zero-padded) whose 1 KB blocks are MFMA operand fragments, which the down
+// GEMM then loads as whole contiguous kilobytes.  Such an h holds
+// chunk_capacity(groups, total_rows) chunks of 32 x N; N and the down GEMM's
+// K must be multiples of 16.
+size_t chunk_capacity(int groups, int total_rows);
+constexpr int kChunkRowsHost = 32;  // rows of a chunk of the blocked layout
 
 // y[r][n] = sum_c h[r][c] Wd(g, n, c), h row stride K, y row stride N.
 // Wd(g, n, c) = w[g*group_stride + (c / kseg)*seg_stride + n*ldw + c % kseg]
@@ -72,6 +83,8 @@ struct DownArgs {
   uint16_t* y;
   int K, N, kseg, ldw;
   size_t seg_stride, group_stride;
+  // h in the chunk-blocked layout written by launch_ffn_up
+  bool h_blocked;
 };
 hipError_t launch_ffn_down(const Segments& seg, const DownArgs& a, hipStream_t st);
 

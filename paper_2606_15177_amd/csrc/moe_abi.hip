@@ -36,12 +36,42 @@ int64_t sh_width(const moe_dims* d) {
   return d->n_shared > 0 ? static_cast<int64_t>(d->n_shared) * d->I_shared : 0;
 }
 
-size_t ffn_ws(const moe_dims* d) {
-  const size_t rows = static_cast<size_t>(d->T) * d->k;
-  size_t b = align_up(rows * d->I * sizeof(uint16_t));                           // h
-  b += align_up(static_cast<size_t>(d->T) * sh_width(d) * sizeof(uint16_t));   // h_shared
-  return b;
+// Decode-sized batches run the routed GEMMs on chunk-blocked activations.
+bool ffn_blocked(const moe_dims* d) {
+  const moe::Segments routed{nullptr, d->E_local, 0, d->T, d->T * d->k};
+  return d->T > 0 && moe::ffn_up_reads_rows(routed) && d->H % 16 == 0 && d->I % 16 == 0;
 }
+
+// Workspace of the expert FFN: h (chunk-blocked for decode-sized batches),
+// then h_shared.
+struct FfnWs {
+  uint16_t* h;
+  bool h_blocked;
+  uint16_t* h_sh;
+  size_t bytes;
+};
+FfnWs carve_ffn(const moe_dims* d, void* base) {
+  FfnWs w{};
+  unsigned char* p = static_cast<unsigned char*>(base);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    unsigned char* r = p ? p + off : nullptr;
+    off += align_up(bytes);
+    return r;
+  };
+  const size_t rows = static_cast<size_t>(d->T) * d->k;
+  w.h_blocked = ffn_blocked(d);
+  if (w.h_blocked) {
+    const size_t chunk_rows = moe::chunk_capacity(d->E_local, static_cast<int>(rows)) * moe::kChunkRowsHost;
+    w.h = reinterpret_cast<uint16_t*>(take(chunk_rows * d->I * sizeof(uint16_t)));
+  } else {
+    w.h = reinterpret_cast<uint16_t*>(take(rows * d->I * sizeof(uint16_t)));
+  }
+  w.h_sh = reinterpret_cast<uint16_t*>(take(static_cast<size_t>(d->T) * sh_width(d) * sizeof(uint16_t)));
+  w.bytes = off;
+  return w;
+}
+size_t ffn_ws(const moe_dims* d) { return carve_ffn(d, nullptr).bytes; }
 
 // The forward workspace, carved in this order.
 struct ForwardWs {
@@ -125,32 +155,31 @@ int weights_ok(const moe_dims* d, const moe_weights* w) {
 int run_ffn(const moe_dims* d, const uint16_t* x_perm, const int32_t* x_rows, const int32_t* offsets,
             const moe_weights* w, const uint16_t* x, uint16_t* y_perm, uint16_t* y_shared,
             void* ws, const moe_taps* taps, hipStream_t st) {
-  const size_t rows = static_cast<size_t>(d->T) * d->k;
-  uint16_t* h = static_cast<uint16_t*>(ws);
-  uint16_t* h_sh = reinterpret_cast<uint16_t*>(static_cast<unsigned char*>(ws) +
-                                               align_up(rows * d->I * sizeof(uint16_t)));
+  const FfnWs fw = carve_ffn(d, ws);
+  uint16_t* h = fw.h;
+  uint16_t* h_sh = fw.h_sh;
   const int shw = static_cast<int>(sh_width(d));
   const moe::Segments routed{offsets, d->E_local, 0, d->T, d->T * d->k};
   const moe::Segments shared{nullptr, 1, d->T, d->T, d->T};
   hipError_t e;
 
   record(taps, 2 * MOE_STAGE_FFN_UP, st);
-  e = moe::launch_ffn_up(routed, moe::UpArgs{x_perm, w->w_gate, w->w_up, h, d->H, d->I, x_rows}, st);
+  e = moe::launch_ffn_up(routed, moe::UpArgs{x_perm, w->w_gate, w->w_up, h, d->H, d->I, x_rows, fw.h_blocked}, st);
   if (e != hipSuccess) return MOE_ERR_DEVICE;
   if (d->n_shared > 0) {
-    e = moe::launch_ffn_up(shared, moe::UpArgs{x, w->sh_gate, w->sh_up, h_sh, d->H, shw, nullptr}, st);
+    e = moe::launch_ffn_up(shared, moe::UpArgs{x, w->sh_gate, w->sh_up, h_sh, d->H, shw, nullptr, false}, st);
     if (e != hipSuccess) return MOE_ERR_DEVICE;
   }
   record(taps, 2 * MOE_STAGE_FFN_UP + 1, st);
 
   record(taps, 2 * MOE_STAGE_FFN_DOWN, st);
   moe::DownArgs dn{h, w->w_down, y_perm, d->I, d->H, d->I, d->I, 0,
-                   static_cast<size_t>(d->H) * d->I};
+                   static_cast<size_t>(d->H) * d->I, fw.h_blocked};
   e = moe::launch_ffn_down(routed, dn, st);
   if (e != hipSuccess) return MOE_ERR_DEVICE;
   if (d->n_shared > 0) {
     moe::DownArgs ds{h_sh, w->sh_down, y_shared, shw, d->H, d->I_shared, d->I_shared,
-                     static_cast<size_t>(d->H) * d->I_shared, 0};
+                     static_cast<size_t>(d->H) * d->I_shared, 0, false};
     e = moe::launch_ffn_down(shared, ds, st);
     if (e != hipSuccess) return MOE_ERR_DEVICE;
   }
