@@ -180,7 +180,7 @@ def make_taps(topk_idx=None, topk_w=None, expert_load=None, offsets=None, perm_t
                 _ptr(offsets, _I32), _ptr(perm_token, _I32), _ptr(inv_pos, _I32))
     if events is not None:
         for i, e in enumerate(events):
-            t.events[i] = e
+            t.events[i] = e  # None leaves the slot empty: that stage is not recorded
     return t
 
 
