@@ -4,12 +4,15 @@
 // A stable counting sort of the T*k pairs by local slot, in three launches
 // over tiles of kTile consecutive pairs (token-major order):
 //   1. count   per tile and slot, LDS atomics -> tile_counts[tile][slot];
-//   2. scan    one block: per-slot exclusive prefix over tiles (in place) and
-//              the exclusive prefix over slots -> offsets[0..E_local];
-//   3. scatter one wave per tile walks its pairs in order, 64 at a time; the
-//              pairs of one slot inside a 64-pair chunk are ranked with a
-//              ballot + popcount, so ties keep token order without depending
-//              on atomic order.  Writes perm_token and inv_pos.
+//   2. scan    one block per slot: exclusive prefix over the tiles (in
+//              place) and the slot's total;
+//   3. scatter one block of kTile/64 waves per tile, a 64-pair chunk per
+//              wave: the pairs of one slot inside a chunk are ranked with a
+//              ballot + popcount and the chunks of a tile are chained by a
+//              per-slot prefix over the waves, so ties keep token order
+//              without depending on atomic order.  Each block also derives
+//              the slot offsets from the totals (block 0 stores them).
+//              Writes perm_token and inv_pos.
 // When all pairs fit in one tile (decode-sized batches) a single one-block
 // kernel does the three steps.  The row gather x_perm[r] = x[perm_token[r]]
 // is a separate, bandwidth-bound kernel that copies 16-byte vectors.
@@ -126,39 +129,84 @@ __device__ int block_exclusive_scan(int v, int* total) {
   return before + inc - v;
 }
 
-__global__ __launch_bounds__(1024) void perm_scan_kernel(int n_tiles, int E_local,
-                                                         int32_t* __restrict__ tile_counts,
-                                                         int32_t* __restrict__ offsets) {
-  const int s = threadIdx.x;
-  int running = 0;
-  if (s < E_local) {
-    for (int tile = 0; tile < n_tiles; ++tile) {
-      const size_t i = static_cast<size_t>(tile) * E_local + s;
-      const int c = tile_counts[i];
-      tile_counts[i] = running;
-      running += c;
-    }
+__global__ __launch_bounds__(256) void perm_scan_kernel(int n_tiles, int E_local,
+                                                        int32_t* __restrict__ tile_counts,
+                                                        int32_t* __restrict__ slot_total) {
+  const int s = blockIdx.x;
+  int carry = 0;
+  for (int t0 = 0; t0 < n_tiles; t0 += blockDim.x) {
+    const int t = t0 + threadIdx.x;
+    const size_t i = static_cast<size_t>(t) * E_local + s;
+    const int v = t < n_tiles ? tile_counts[i] : 0;
+    int total;
+    const int ex = block_exclusive_scan(v, &total);
+    if (t < n_tiles) tile_counts[i] = carry + ex;
+    carry += total;
   }
-  int total;
-  const int excl = block_exclusive_scan(running, &total);
-  if (s < E_local) offsets[s] = excl;
-  if (s == 0) offsets[E_local] = total;
+  if (threadIdx.x == 0) slot_total[s] = carry;
 }
 
-__global__ __launch_bounds__(kWave) void perm_scatter_kernel(
+constexpr int kScatterWaves = kTile / kWave;
+
+__global__ __launch_bounds__(kTile) void perm_scatter_kernel(
     int n_pairs, int k, int E, int E_local, const int32_t* __restrict__ local_experts,
     const int32_t* __restrict__ topk_idx, const int32_t* __restrict__ tile_prefix,
-    const int32_t* __restrict__ offsets, int32_t* __restrict__ perm_token,
-    int32_t* __restrict__ inv_pos) {
+    const int32_t* __restrict__ slot_total, int32_t* __restrict__ offsets,
+    int32_t* __restrict__ perm_token, int32_t* __restrict__ inv_pos) {
   extern __shared__ int sm[];
   int* slot_of = sm;
-  int* next = sm + E;  // next free row of each slot for this tile
+  int* base = sm + E;               // first row of each slot for this tile
+  int* cnt = base + E_local;        // [wave][slot]: chunk counts, then prefix over waves
   const int tile = blockIdx.x;
-  for (int s = threadIdx.x; s < E_local; s += kWave)
-    next[s] = offsets[s] + tile_prefix[static_cast<size_t>(tile) * E_local + s];
+  const int wave = threadIdx.x / kWave, lane = lane_id();
+  for (int i = threadIdx.x; i < kScatterWaves * E_local; i += blockDim.x) cnt[i] = 0;
   build_slot_map(slot_of, E, E_local, local_experts);
-  for (int c0 = tile * kTile; c0 < min(n_pairs, (tile + 1) * kTile); c0 += kWave)
-    scatter_chunk(c0 + lane_id(), n_pairs, k, E, slot_of, next, topk_idx, perm_token, inv_pos);
+  // slot offsets: exclusive scan of the totals
+  int carry = 0;
+  for (int s0 = 0; s0 < E_local; s0 += blockDim.x) {
+    const int s = s0 + threadIdx.x;
+    int total;
+    const int ex = block_exclusive_scan(s < E_local ? slot_total[s] : 0, &total);
+    if (s < E_local) {
+      base[s] = carry + ex + tile_prefix[static_cast<size_t>(tile) * E_local + s];
+      if (tile == 0) offsets[s] = carry + ex;
+    }
+    carry += total;
+  }
+  if (tile == 0 && threadIdx.x == 0) offsets[E_local] = carry;
+  // rank of each pair among its chunk's pairs of the same slot
+  const int p = tile * kTile + wave * kWave + lane;
+  int s = -1;
+  if (p < n_pairs) {
+    s = slot_lookup(slot_of, topk_idx[p], E);
+    if (s < 0) inv_pos[p] = -1;
+  }
+  const uint64_t below = (1ull << lane) - 1ull;
+  int rank = 0;
+  uint64_t pending = __ballot(s >= 0);
+  while (pending) {
+    const int leader = __ffsll(static_cast<long long>(pending)) - 1;
+    const int sl = __shfl(s, leader);
+    const uint64_t same = __ballot(s == sl);
+    if (s == sl) rank = __popcll(same & below);
+    if (lane == leader) cnt[wave * E_local + sl] = __popcll(same);
+    pending &= ~same;
+  }
+  __syncthreads();
+  for (int sl = threadIdx.x; sl < E_local; sl += blockDim.x) {
+    int run = 0;
+    for (int w = 0; w < kScatterWaves; ++w) {
+      const int c = cnt[w * E_local + sl];
+      cnt[w * E_local + sl] = run;
+      run += c;
+    }
+  }
+  __syncthreads();
+  if (s >= 0) {
+    const int pos = base[s] + cnt[wave * E_local + s] + rank;
+    perm_token[pos] = p / k;
+    inv_pos[p] = pos;
+  }
 }
 
 // All three steps for n_pairs <= kTile in one block of 1024 threads.
@@ -211,7 +259,7 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(int H, const int32_t* 
 
 size_t permute_ws_bytes(int T, int k, int E_local) {
   const size_t n_tiles = static_cast<size_t>(ceil_div(T * k, kTile));
-  return n_tiles * static_cast<size_t>(E_local) * sizeof(int32_t);
+  return (n_tiles + 1) * static_cast<size_t>(E_local) * sizeof(int32_t);  // tile counts, slot totals
 }
 
 hipError_t launch_permute(int T, int k, int E, int E_local, const int32_t* local_experts,
@@ -231,12 +279,13 @@ hipError_t launch_permute(int T, int k, int E, int E_local, const int32_t* local
                      local_experts, topk_idx, tile_counts);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(1024), 0, st, n_tiles, E_local, tile_counts,
-                     offsets);
+  int32_t* slot_total = tile_counts + static_cast<size_t>(n_tiles) * E_local;
+  hipLaunchKernelGGL(perm_scan_kernel, dim3(E_local), dim3(256), 0, st, n_tiles, E_local, tile_counts, slot_total);
   err = hipGetLastError();
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(perm_scatter_kernel, dim3(n_tiles), dim3(kWave), lds, st, n_pairs, k, E,
-                     E_local, local_experts, topk_idx, tile_counts, offsets, perm_token, inv_pos);
+  const size_t lds_scatter = static_cast<size_t>(E + (1 + kScatterWaves) * E_local) * sizeof(int);
+  hipLaunchKernelGGL(perm_scatter_kernel, dim3(n_tiles), dim3(kTile), lds_scatter, st, n_pairs, k, E, E_local,
+                     local_experts, topk_idx, tile_counts, slot_total, offsets, perm_token, inv_pos);
   return hipGetLastError();
 }
 
