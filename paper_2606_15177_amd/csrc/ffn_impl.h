@@ -27,6 +27,7 @@ namespace moe {
 struct GemmArgs {
   const uint16_t* x;
   const int32_t* x_rows;
+  int x_row_count;  // rows of x when x_rows is set
   bool x_blocked, out_blocked;
   const int32_t* offsets;  // [groups+1] device, or nullptr for one group of static_rows
   int static_rows;

@@ -190,12 +190,23 @@ __global__ __launch_bounds__(kThreads) void tiled_kernel(GemmArgs a) {
     }
     const TileInfo ti = tile_info(t);
     if (grp == 0) {
-      rs_ld = __builtin_amdgcn_make_buffer_rsrc(
-          const_cast<uint16_t*>(a.x + static_cast<size_t>(ti.row_base + ti.m0) * a.K), 0, kRecords, kRsrcWord3);
+      // token rows: consecutive rows of x, or x rows named by x_rows (the
+      // dispatch gather done by the loads themselves)
+      const uint16_t* xb = a.x_rows ? a.x : a.x + static_cast<size_t>(ti.row_base + ti.m0) * a.K;
+      rs_ld = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(xb), 0, kRecords, kRsrcWord3);
+      // the four row indices are loaded together (rows past the group read
+      // the group's first index and are masked), so one wait covers them
+      int xr[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int r = 16 * (4 * q + i) + (lane >> 2);  // token row within the tile
-        ld_off[i] = (ti.m0 + r < ti.m) ? static_cast<uint32_t>(r * a.K * 2 + chunk * 16) : kInvalid;
+        xr[i] = r;
+        if (a.x_rows) xr[i] = a.x_rows[ti.row_base + (ti.m0 + r < ti.m ? ti.m0 + r : 0)];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = 16 * (4 * q + i) + (lane >> 2);
+        ld_off[i] = ti.m0 + r < ti.m ? static_cast<uint32_t>(xr[i] * a.K * 2 + chunk * 16) : kInvalid;
       }
     } else {
       const int col0 = ti.nt * OUT_COLS;
@@ -402,22 +413,25 @@ hipError_t launch_tiled_t(const Segments& seg, const GemmArgs& a, hipStream_t st
 }  // namespace
 
 hipError_t launch_tiled(const Segments& seg, const GemmArgs& a, bool gated, hipStream_t st) {
-  if (seg.groups > kMaxGroups || a.x_rows != nullptr || a.x_blocked || a.out_blocked) return hipErrorInvalidValue;
-  // 32-bit byte offsets: a tile's X rows and a group's weight columns
-  const size_t x_span = static_cast<size_t>(kBM) * a.K * 2;
+  if (seg.groups > kMaxGroups || a.x_blocked || a.out_blocked) return hipErrorInvalidValue;
+  // 32-bit byte offsets: a tile's X rows (all of x when rows are indexed) and
+  // a group's weight columns
+  const size_t x_span = static_cast<size_t>(a.x_rows ? a.x_row_count : kBM) * a.K * 2;
   const size_t w_span = (static_cast<size_t>(kBN) * a.ldw +
                          (a.kseg < a.K ? static_cast<size_t>((a.K - 1) / a.kseg) * a.seg_stride : 0) + a.K) * 2;
   if (x_span >= 0x80000000ull || w_span >= 0x80000000ull) return hipErrorInvalidValue;
   return gated ? launch_tiled_t<true>(seg, a, st) : launch_tiled_t<false>(seg, a, st);
 }
 
-bool ffn_up_reads_rows(const Segments& seg) { return seg.max_rows <= kSkinnyMaxRows; }
+bool ffn_streams_weights(const Segments& seg) { return seg.max_rows <= kSkinnyMaxRows; }
 
 hipError_t launch_ffn_up(const Segments& seg, const UpArgs& u, hipStream_t st) {
-  if ((u.x_rows || u.h_blocked) && !ffn_up_reads_rows(seg)) return hipErrorInvalidValue;
+  if (u.h_blocked && !ffn_streams_weights(seg)) return hipErrorInvalidValue;
+  if (u.x_rows && (seg.offsets == nullptr || u.x_row_count <= 0)) return hipErrorInvalidValue;
   GemmArgs a{};
   a.x = u.x;
   a.x_rows = u.x_rows;
+  a.x_row_count = u.x_row_count;
   a.out_blocked = u.h_blocked;
   a.offsets = seg.offsets;
   a.static_rows = seg.static_rows;
@@ -436,7 +450,7 @@ hipError_t launch_ffn_up(const Segments& seg, const UpArgs& u, hipStream_t st) {
 }
 
 hipError_t launch_ffn_down(const Segments& seg, const DownArgs& d, hipStream_t st) {
-  if (d.h_blocked && !ffn_up_reads_rows(seg)) return hipErrorInvalidValue;
+  if (d.h_blocked && !ffn_streams_weights(seg)) return hipErrorInvalidValue;
   GemmArgs a{};
   a.x = d.h;
   a.x_blocked = d.h_blocked;

@@ -48,7 +48,7 @@ struct Segments {
 // h[r][i] = silu(sum_c X[r][c] Wg[g][i][c]) * (sum_c X[r][c] Wu[g][i][c]),
 // weights [groups][N][K] (group stride N*K), x row stride K, h row stride N.
 // X[r] = x[r], or x[x_rows[r]] when x_rows != nullptr (the dispatch gather
-// read in place); x_rows is accepted only when ffn_up_reads_rows(seg).
+// read in place; x then has x_row_count rows).
 struct UpArgs {
   const uint16_t* x;
   const uint16_t* w_gate;
@@ -56,15 +56,16 @@ struct UpArgs {
   uint16_t* h;
   int K, N;
   const int32_t* x_rows;
+  int x_row_count;
   // write h in the chunk-blocked layout (decode-sized groups, see below)
   bool h_blocked;
 };
 hipError_t launch_ffn_up(const Segments& seg, const UpArgs& a, hipStream_t st);
-// True when the gate/up GEMM for these segments can read its rows through an
-// index (the weight-streaming kernel for decode-sized groups).
-bool ffn_up_reads_rows(const Segments& seg);
+// True when these segments take the weight-streaming kernels (decode-sized
+// groups).
+bool ffn_streams_weights(const Segments& seg);
 
-// For decode-sized groups (ffn_up_reads_rows) the gate/up GEMM may write h
+// For decode-sized groups (ffn_streams_weights) the gate/up GEMM may write h
 // chunk-blocked: each group's rows cut into chunks of 32 (the last one
 // zero-padded) whose 1 KB blocks are MFMA operand fragments, which the down
 // GEMM then loads as whole contiguous kilobytes.  Such an h holds

@@ -39,7 +39,7 @@ int64_t sh_width(const moe_dims* d) {
 // Decode-sized batches run the routed GEMMs on chunk-blocked activations.
 bool ffn_blocked(const moe_dims* d) {
   const moe::Segments routed{nullptr, d->E_local, 0, d->T, d->T * d->k};
-  return d->T > 0 && moe::ffn_up_reads_rows(routed) && d->H % 16 == 0 && d->I % 16 == 0;
+  return d->T > 0 && moe::ffn_streams_weights(routed) && d->H % 16 == 0 && d->I % 16 == 0;
 }
 
 // Workspace of the expert FFN: h (chunk-blocked for decode-sized batches),
@@ -80,7 +80,6 @@ struct ForwardWs {
   int32_t* offsets;
   int32_t* perm_token;
   int32_t* inv_pos;
-  uint16_t* x_perm;
   uint16_t* y_perm;
   uint16_t* y_shared;
   void* permute_ws;
@@ -103,7 +102,6 @@ ForwardWs carve_forward(const moe_dims* d, void* base) {
   w.offsets = reinterpret_cast<int32_t*>(take((d->E_local + 1) * sizeof(int32_t)));
   w.perm_token = reinterpret_cast<int32_t*>(take(rows * sizeof(int32_t)));
   w.inv_pos = reinterpret_cast<int32_t*>(take(rows * sizeof(int32_t)));
-  w.x_perm = reinterpret_cast<uint16_t*>(take(rows * d->H * sizeof(uint16_t)));
   w.y_perm = reinterpret_cast<uint16_t*>(take(rows * d->H * sizeof(uint16_t)));
   w.y_shared = reinterpret_cast<uint16_t*>(
       take(d->n_shared > 0 ? static_cast<size_t>(d->T) * d->H * sizeof(uint16_t) : 0));
@@ -164,10 +162,11 @@ int run_ffn(const moe_dims* d, const uint16_t* x_perm, const int32_t* x_rows, co
   hipError_t e;
 
   record(taps, 2 * MOE_STAGE_FFN_UP, st);
-  e = moe::launch_ffn_up(routed, moe::UpArgs{x_perm, w->w_gate, w->w_up, h, d->H, d->I, x_rows, fw.h_blocked}, st);
+  e = moe::launch_ffn_up(routed, moe::UpArgs{x_perm, w->w_gate, w->w_up, h, d->H, d->I, x_rows, d->T, fw.h_blocked},
+                         st);
   if (e != hipSuccess) return MOE_ERR_DEVICE;
   if (d->n_shared > 0) {
-    e = moe::launch_ffn_up(shared, moe::UpArgs{x, w->sh_gate, w->sh_up, h_sh, d->H, shw, nullptr, false}, st);
+    e = moe::launch_ffn_up(shared, moe::UpArgs{x, w->sh_gate, w->sh_up, h_sh, d->H, shw, nullptr, 0, false}, st);
     if (e != hipSuccess) return MOE_ERR_DEVICE;
   }
   record(taps, 2 * MOE_STAGE_FFN_UP + 1, st);
@@ -328,19 +327,11 @@ int moe_forward(const moe_dims* d, const float* logits, const int32_t* src, cons
   e = moe::launch_permute(d->T, d->k, d->E, d->E_local, local_experts, topk_idx, offsets,
                           perm_token, inv_pos, fw.permute_ws, st);
   if (e != hipSuccess) return MOE_ERR_DEVICE;
-  // decode-sized groups: the gate/up kernel reads x through perm_token
-  // instead of a gathered copy
-  const moe::Segments routed_seg{offsets, d->E_local, 0, d->T, d->T * d->k};
-  const bool direct = moe::ffn_up_reads_rows(routed_seg);
-  if (!direct) {
-    e = moe::launch_gather_rows(d->T * d->k, d->H, perm_token, offsets + d->E_local, x, fw.x_perm, st);
-    if (e != hipSuccess) return MOE_ERR_DEVICE;
-  }
+  // no gathered copy of x: the gate/up GEMM reads its rows through perm_token
   record(taps, 2 * MOE_STAGE_PERMUTE + 1, st);
 
   if (d->T > 0) {
-    s = run_ffn(d, direct ? x : fw.x_perm, direct ? perm_token : nullptr, offsets, w, x, fw.y_perm,
-                fw.y_shared, fw.ffn_ws, taps, st);
+    s = run_ffn(d, x, perm_token, offsets, w, x, fw.y_perm, fw.y_shared, fw.ffn_ws, taps, st);
     if (s != MOE_OK) return s;
   } else {
     record(taps, 2 * MOE_STAGE_FFN_UP, st);
