@@ -86,8 +86,9 @@ def stage_work(cfg, R: int, active: int) -> dict:
     bf = 2
     w = {}
     w["route"] = dict(bytes=T * E * 4 + T * 4 + T * k * 8 + 2 * S * E * 8, flops=0)
-    w["permute"] = dict(bytes=T * k * 4 + (cfg.E_local + 1) * 4 + R * 4 + T * k * 4 + 2 * R * H * bf,
-                        flops=0)
+    # the dispatch sort only: the token rows are read by the gate/up GEMM
+    # through perm_token (counted there as R*H*bf), never copied
+    w["permute"] = dict(bytes=T * k * 4 + (cfg.E_local + 1) * 4 + R * 4 + T * k * 4, flops=0)
     w["ffn_up"] = dict(bytes=active * 2 * I * H * bf + n_sh * 2 * I_sh * H * bf + R * H * bf
                        + (T * H * bf if n_sh else 0) + R * I * bf + T * n_sh * I_sh * bf,
                        flops=2 * 2 * H * I * R + 2 * 2 * H * n_sh * I_sh * T)

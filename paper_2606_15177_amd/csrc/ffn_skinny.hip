@@ -29,7 +29,7 @@ namespace {
 constexpr uint32_t kInvalidOff = 0x80000000u;  // past the descriptor's range: reads zeros, no traffic
 
 // 64 lanes x 16 bytes from rs + off[lane] to lds + 16 * lane.
-__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t rs, unsigned char* lds, uint32_t off) {
+__device__ __forceinline__ void stream_lds16(__amdgpu_buffer_rsrc_t rs, unsigned char* lds, uint32_t off) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)lds, 16, off, 0, 0, 0);
 }
 
@@ -116,9 +116,9 @@ __global__ __launch_bounds__(KP* kWave) void skinny_kernel(GemmArgs a) {
       for (int b = 0; b < NB; ++b) {
         const uint32_t off = kok ? roff[b][i] + col : kInvalidOff;
         if (GATED && b == 1)
-          load_lds16(rs1, dst + b * STEPB + i * 1024, off);
+          stream_lds16(rs1, dst + b * STEPB + i * 1024, off);
         else
-          load_lds16(rs0, dst + b * STEPB + i * 1024, off);
+          stream_lds16(rs0, dst + b * STEPB + i * 1024, off);
       }
     }
   };
