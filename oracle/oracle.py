@@ -2,9 +2,10 @@
 
 TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the benchmark's CPU
 baseline may use this module; the product path never imports it.  It only
-marshals numpy arrays into ``moe_oracle.c``, where all the arithmetic lives
-(fp64, single-threaded, written from the definitions).  Shares nothing with
-the HIP library.
+marshals numpy arrays into ``moe_oracle.c`` (the layer) and ``place_oracle.c``
+(source-aware expert placement), where all the arithmetic lives (fp64,
+single-threaded, written from the definitions).  Shares nothing with the HIP
+library.
 """
 from __future__ import annotations
 
@@ -15,7 +16,7 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-SRC = os.path.join(_HERE, "moe_oracle.c")
+SRCS = [os.path.join(_HERE, "moe_oracle.c"), os.path.join(_HERE, "place_oracle.c")]
 # MOE_ORACLE_LIB lets the mutation test load a deliberately broken build.
 LIB = os.environ.get("MOE_ORACLE_LIB") or os.path.join(_HERE, "libmoe_oracle.so")
 
@@ -28,11 +29,13 @@ _vp = C.c_void_p
 
 
 def build(force: bool = True) -> str:
-    """Compile the oracle with gcc (plain -O2: no fast-math, no host-specific ISA)."""
+    """Compile the oracle with gcc (plain -O2: no fast-math, no host-specific
+    ISA, no contraction into fused multiply-adds, so every fp64 operation
+    rounds as written)."""
     if force or not os.path.exists(LIB):
         tmp = LIB + ".tmp"
-        subprocess.check_call(["gcc", "-O2", "-std=c99", "-fPIC", "-shared",
-                               "-Wall", "-Wextra", SRC, "-o", tmp, "-lm"])
+        subprocess.check_call(["gcc", "-O2", "-std=c99", "-ffp-contract=off", "-fPIC", "-shared",
+                               "-Wall", "-Wextra", *SRCS, "-o", tmp, "-lm"])
         os.replace(tmp, LIB)
     return LIB
 
@@ -57,7 +60,11 @@ def lib():
         L.oracle_combine.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int, _u16p, _i32p, _f32p, _vp, _f64p]
         L.oracle_forward_tokens.argtypes = [_i32p, C.c_int, _i32p, _f32p, _u16p, _vp, _u16p, _u16p, _u16p,
                                             _vp, _vp, _vp, _f64p]
-        for name in ("oracle_route", "oracle_route_stats", "oracle_permute", "oracle_gather_rows",
+        L.oracle_place_objective.argtypes = [C.c_int] * 4 + [_i64p, _vp, _f64p, _vp, C.c_double, _i32p,
+                                                             _i32p, _f64p]
+        L.oracle_place_greedy.argtypes = [C.c_int] * 4 + [_i64p, _vp, _f64p, _vp, C.c_double, _i32p, _i32p,
+                                                          C.c_double, C.c_double, C.c_double, _i32p, _vp]
+        for name in ("oracle_place_objective", "oracle_place_greedy", "oracle_route", "oracle_route_stats", "oracle_permute", "oracle_gather_rows",
                      "oracle_swiglu_hidden", "oracle_linear", "oracle_swiglu_ffn", "oracle_ffn_rows",
                      "oracle_combine", "oracle_forward_tokens"):
             getattr(L, name).restype = C.c_int
@@ -196,3 +203,43 @@ def forward_tokens(dims: dict, tokens, logits, x, local_experts, weights: dict) 
                                        _c(weights["w_up"], np.uint16), _c(weights["w_down"], np.uint16),
                                        _ptr(shg), _ptr(shu), _ptr(shd), out), "oracle_forward_tokens")
     return out[: len(tokens)]
+
+
+# ---- source-aware expert placement (Sec. 5.2 objective, Sec. 5.3 greedy) ----
+
+def _place_inputs(A, B, D, M, x0):
+    A = _c(A, np.int64)
+    if A.ndim == 2:
+        A = A[None]
+    L, S, E = A.shape
+    D = _c(D, np.float64)
+    G = D.shape[1]
+    assert D.shape == (S, G)
+    B = None if B is None else _c(B, np.int64).reshape(L, E)
+    M = None if M is None else _c(M, np.float64).reshape(L, E, G)
+    x0 = _c(x0, np.int32).reshape(L, E)
+    return A, B, D, M, x0, (L, S, E, G)
+
+
+def place_objective(A, D, x, x0, B=None, M=None, m_uniform: float = 1.0) -> np.ndarray:
+    """[L, 3] = (C_comm, C_load, C_mig) of placement x (rank per expert, [L, E])."""
+    A, B, D, M, x0, (L, S, E, G) = _place_inputs(A, B, D, M, x0)
+    x = _c(x, np.int32).reshape(L, E)
+    terms = np.empty((max(L, 1), 3), np.float64)
+    _check(lib().oracle_place_objective(L, S, E, G, A, _ptr(B), D, _ptr(M), float(m_uniform), x0, x, terms),
+           "oracle_place_objective")
+    return terms[:L]
+
+
+def place_greedy(A, D, x0, cap, B=None, M=None, m_uniform: float = 1.0,
+                 alpha: float = 1.0, beta: float = 0.0025, gamma: float = 1.0):
+    """(x [L, E] rank per expert, step_score [L, E]) of the online greedy."""
+    A, B, D, M, x0, (L, S, E, G) = _place_inputs(A, B, D, M, x0)
+    cap = _c(cap, np.int32)
+    assert cap.shape == (G,)
+    x = np.empty((max(L, 1), E), np.int32)
+    score = np.empty((max(L, 1), E), np.float64)
+    _check(lib().oracle_place_greedy(L, S, E, G, A, _ptr(B), D, _ptr(M), float(m_uniform), x0, cap,
+                                     float(alpha), float(beta), float(gamma), x, _ptr(score)),
+           "oracle_place_greedy")
+    return x[:L], score[:L]

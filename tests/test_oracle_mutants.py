@@ -8,8 +8,10 @@ import sys
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-SRC = os.path.join(ROOT, "oracle", "moe_oracle.c")
-PINS = os.path.join(ROOT, "tests", "test_oracle_pins.py")
+ORACLE = os.path.join(ROOT, "oracle")
+LAYER_SRC, PLACE_SRC = "moe_oracle.c", "place_oracle.c"
+PINS = {LAYER_SRC: os.path.join(ROOT, "tests", "test_oracle_pins.py"),
+        PLACE_SRC: os.path.join(ROOT, "tests", "test_place_pins.py")}
 
 # (name, text to replace, replacement, which occurrence (0-based))
 MUTANTS = [
@@ -36,6 +38,33 @@ MUTANTS = [
     ("shared_dropped", "for (int q = 0; q < n_sh; ++q) {", "for (int q = 0; q < 0; ++q) {", 0),
     ("combine_weight_dropped", "o[c] += w * bf16_value(", "o[c] += bf16_value(", 0),
 ]
+LAYER_MUTANTS = [(LAYER_SRC,) + m for m in MUTANTS]
+
+PLACE_MUTANTS = [(PLACE_SRC,) + m for m in [
+    ("coldest_first", "return Ba > Bb;", "return Ba < Bb;", 0),
+    ("volume_ignored", "return Va > Vb;", "return a < b;", 0),
+    ("load_term_sign", "double c_load = v * v - u * u;", "double c_load = u * u - v * v;", 0),
+    ("load_term_without_expert", "double v = (double)(load[g] + Bl[e]) - mean;",
+     "double v = (double)load[g] - mean;", 0),
+    ("load_term_absolute", "double c_load = v * v - u * u;", "double c_load = v * v;", 0),
+    ("mean_over_experts", "double mean = (double)total / G;", "double mean = (double)total / E;", 0),
+    ("old_rank_not_charged", "c_mig = c_mig + mig_cost(M, m_uniform, l, E, G, e, home);",
+     "c_mig = c_mig + 0.0;", 0),
+    ("comm_d_transposed", "(double)Al[(size_t)s * E + e] * D[(size_t)s * G + g];",
+     "(double)Al[(size_t)s * E + e] * D[(size_t)(g % S) * G + (s % G)];", 0),
+    ("comm_a_transposed", "c_comm = c_comm + (double)Al[(size_t)s * E + e]",
+     "c_comm = c_comm + (double)Al[(size_t)(e % S) * E + (s % E)]", 0),
+    ("tie_prefers_moving", "take = g == home;", "take = g != home;", 0),
+    ("tie_prefers_fuller", "take = n[g] < n[best];", "take = n[g] > n[best];", 0),
+    ("tie_to_higher_rank", "take = g < best;", "take = g > best;", 0),
+    ("capacity_off_by_one", "if (n[g] >= cap[g])", "if (n[g] > cap[g])", 0),
+    ("nan_wins", "score = INFINITY;", "score = -INFINITY;", 0),
+    ("beta_dropped", "score = score + beta * c_load;", "score = score + c_load;", 0),
+    ("objective_mean_wrong", "mean /= G;", "mean /= (G + 1);", 0),
+    ("objective_mig_signed", "* fabs(xi - x0i);", "* (xi - x0i);", 0),
+    ("objective_comm_ignores_x", "D[(size_t)s * G + g] *\n                              (xl[e] == g ? 1.0 : 0.0);",
+     "D[(size_t)s * G + g] *\n                              (xl[e] == g ? 1.0 : 1.0);", 0),
+]]
 
 
 def _mutate(src: str, old: str, new: str, nth: int) -> str:
@@ -46,17 +75,26 @@ def _mutate(src: str, old: str, new: str, nth: int) -> str:
     return src[:pos] + new + src[pos + len(old):]
 
 
-@pytest.mark.parametrize("name,old,new,nth", MUTANTS, ids=[m[0] for m in MUTANTS])
-def test_pins_catch_mutant(tmp_path, name, old, new, nth):
-    with open(SRC) as f:
-        src = f.read()
-    mutated = _mutate(src, old, new, nth)
-    assert mutated != src
-    c = tmp_path / "mutant.c"
-    c.write_text(mutated)
+ALL = LAYER_MUTANTS + PLACE_MUTANTS
+
+
+@pytest.mark.parametrize("src_name,name,old,new,nth", ALL, ids=[m[1] for m in ALL])
+def test_pins_catch_mutant(tmp_path, src_name, name, old, new, nth):
+    sources = []
+    for fname in (LAYER_SRC, PLACE_SRC):
+        with open(os.path.join(ORACLE, fname)) as f:
+            src = f.read()
+        if fname == src_name:
+            mutated = _mutate(src, old, new, nth)
+            assert mutated != src
+            src = mutated
+        c = tmp_path / fname
+        c.write_text(src)
+        sources.append(str(c))
     so = tmp_path / "libmutant.so"
-    subprocess.check_call(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", str(c), "-o", str(so), "-lm"])
+    subprocess.check_call(["gcc", "-O2", "-std=c99", "-ffp-contract=off", "-fPIC", "-shared", *sources,
+                           "-o", str(so), "-lm"])
     env = dict(os.environ, MOE_ORACLE_LIB=str(so))
-    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider", PINS],
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider", PINS[src_name]],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=300)
     assert r.returncode == 1, f"mutant {name} survived the pins:\n{r.stdout[-2000:]}"
