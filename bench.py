@@ -10,6 +10,10 @@ intermediate 14336), inputs and bf16 weights resident in HBM.  Prints one JSON
 line: whole-job tokens/s, per-stage kernel times measured live with HIP
 events on the launch stream, the roofline position of the dominant kernel and
 the CPU oracle's throughput on a bounded sample of the same workload.
+
+With a placement workload (--config place_*), a step is instead one
+moe_place_experts call: the source-aware greedy expert placement of every MoE
+layer of a model from its window statistics, inputs resident in HBM.
 """
 from __future__ import annotations
 
@@ -64,6 +68,12 @@ class HipEvents:
             if rc != 0:
                 raise RuntimeError(f"hipEventCreate failed ({rc})")
             self.ev.append(e.value)
+
+    def record(self, i: int, stream: int) -> None:
+        self.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        rc = self.hip.hipEventRecord(self.ev[i], stream)
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord failed ({rc})")
 
     def elapsed_ms(self, a: int, b: int) -> float:
         ms = ctypes.c_float()
@@ -140,12 +150,95 @@ def cpu_baseline(cfg, wl, budget_s: float) -> dict:
                       f"SwiGLU experts + combine, fp64, single thread ({dt:.1f} s)"}
 
 
+def bench_place(args) -> int:
+    """Latency of one placement call over all layers of the workload."""
+    import numpy as np
+    import torch
+
+    from paper_2606_15177_amd import moe
+    from paper_2606_15177_amd import workloads as W
+
+    cfg = W.PLACE_CONFIGS[args.config]
+    torch.cuda.set_device(0)
+    print(f"[bench] generating {cfg.name} (seed {args.seed})", file=sys.stderr, flush=True)
+    p = W.make_place_inputs(cfg, args.seed)
+    A = torch.from_numpy(p["A"]).cuda()
+    D = torch.from_numpy(p["D"]).cuda()
+    x0 = torch.from_numpy(p["x0"]).cuda()
+    pd = moe.place_dims(cfg.L, cfg.S, cfg.E, cfg.G, *moe.PAPER_PLACE_WEIGHTS, cfg.m_uniform)
+    slots = moe.place_slots(pd, p["cap"])
+    x = torch.empty((cfg.L, cfg.E), dtype=torch.int32, device="cuda")
+    rank_experts = torch.empty((cfg.L, cfg.G, slots), dtype=torch.int32, device="cuda")
+    cost = torch.empty((cfg.L, 3), dtype=torch.float64, device="cuda")
+
+    def call():
+        moe.place_experts(pd, p["cap"], A, D, x0, x, rank_experts=rank_experts, cost=cost)
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        call()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream().cuda_stream
+    events = HipEvents(2 * args.steps)
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        events.record(2 * i, stream)
+        call()
+        events.record(2 * i + 1, stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    kernel_ms = sum(events.elapsed_ms(2 * i, 2 * i + 1) for i in range(args.steps)) / args.steps
+    events.close()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    moved = float((x.cpu().numpy() != p["x0"]).mean())
+    result = {
+        "metric": "expert placement: MoE layers placed per second on 1 MI355X",
+        "value": round(cfg.L / (ms_per_step * 1e-3), 1),
+        "unit": "layers/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "L": cfg.L, "S": cfg.S, "E": cfg.E, "G": cfg.G, "k": cfg.k,
+                   "tokens_per_source": cfg.tokens_per_source, "weights": list(moe.PAPER_PLACE_WEIGHTS),
+                   "parallelism": "single GPU"},
+        # one workgroup per layer, every layer at once: the critical path is
+        # the E dependent placement steps of one layer
+        "roofline": {"bound": "latency", "kernel": "place", "kernel_ms": round(kernel_ms, 4),
+                     "ns_per_expert_step": round(kernel_ms * 1e6 / cfg.E, 1)},
+        "moved_fraction": round(moved, 4),
+        "device": torch.cuda.get_device_name(0),
+    }
+    if not args.no_cpu_baseline:
+        from oracle import oracle
+        oracle.lib()
+        n, t_cpu = 0, 0.0
+        while t_cpu < min(args.cpu_seconds, 5.0) and n < 1000:
+            c0 = time.perf_counter()
+            oracle.place_greedy(p["A"], p["D"], p["x0"], p["cap"], m_uniform=cfg.m_uniform)
+            t_cpu += time.perf_counter() - c0
+            n += 1
+        result["cpu_baseline"] = {
+            "value": round(n * cfg.L / t_cpu, 1), "unit": "layers/s", "cores": 1, "kind": "oracle",
+            "sample": f"{n} whole calls ({cfg.L} layers each) of the C oracle's greedy, fp64, single thread"}
+    print(json.dumps(result), flush=True)
+    return 0
+
+
 def main(argv=None) -> int:
     args = parse_args(argv)
     if args.gpus != 1:
         print(f"bench.py measures one GPU's MoE layer; --gpus {args.gpus} is not supported "
               "(this build runs on a single GPU)", file=sys.stderr)
         return 2
+    if args.config.startswith("place_"):
+        return bench_place(args)
 
     import numpy as np
     import torch

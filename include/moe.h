@@ -51,7 +51,7 @@ enum moe_status {
     MOE_ERR_UNSUPPORTED = -3, /* valid, but beyond the kernels' limits */
     MOE_ERR_WORKSPACE = -4,   /* workspace missing or smaller than required */
     MOE_ERR_DEVICE = -5,      /* a kernel launch failed (e.g. not a gfx950 device) */
-    MOE_ERR_ALIGN = -6        /* a pointer is not 16-byte aligned */
+    MOE_ERR_ALIGN = -6        /* a pointer is not aligned as its entry point requires */
 };
 
 /*
@@ -248,6 +248,79 @@ int moe_forward(const moe_dims *dims, const float *logits, const int32_t *src,
                 const moe_bf16 *x, const int32_t *local_experts,
                 const moe_weights *weights, int64_t *counts, moe_bf16 *out,
                 const moe_taps *taps, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * ---- Source-aware expert placement (Sec. 5.2 objective, Sec. 5.3 greedy) ---
+ *
+ * At the end of a profiling window the placement manager turns the window's
+ * statistics into a new expert placement for every layer.  The objective it
+ * trades off (Sec. 5.2), for one layer with placement x_{e,g} in {0, 1}:
+ *   L_g    = sum_e B_e x_{e,g},  Lbar = (1/G) sum_g L_g
+ *   C_load = sum_g (L_g - Lbar)^2
+ *   C_comm = sum_s sum_e sum_g A_{s,e} D_{s,g} x_{e,g}
+ *   C_mig  = sum_e sum_g M_{e,g} |x_{e,g} - x^0_{e,g}|
+ * The online heuristic (Sec. 5.3) visits the experts hottest first (aggregate
+ * load B descending, then source-aware volume sum_s A descending, then lower
+ * expert index) and gives each one the rank with spare capacity whose score
+ *   S_{e,g} = alpha C^comm_{e,g} + beta C^load_{e,g} + gamma C^mig_{e,g}
+ * is lowest, where each term is the amount by which the matching objective
+ * term grows when e joins g, given the experts placed before it:
+ *   C^comm_{e,g} = sum_s A_{s,e} D_{s,g}                 (summed in s order)
+ *   C^load_{e,g} = (L_g + B_e - Lbar)^2 - (L_g - Lbar)^2 (L_g: load placed on g
+ *                  so far; Lbar = (sum_e B_e) / G, the final average)
+ *   C^mig_{e,g}  = 0 when g = x^0_e, else M_{e,g} + M_{e,x^0_e} (the second
+ *                  term only when x^0_e is a rank)
+ * Equal scores go to the expert's current rank, then to the rank with fewer
+ * experts placed so far, then to the lower rank index.  Scores are fp64,
+ * evaluated exactly in the order written (alpha C^comm, + beta C^load,
+ * + gamma C^mig) without fused multiply-adds; a NaN score counts as +inf.
+ * The paper calibrates (alpha, beta, gamma) = (1.0, 0.0025, 1.0) (Sec. 6).
+ */
+typedef struct moe_place_dims {
+    int32_t L;    /* layers placed by one call, >= 0 */
+    int32_t S;    /* source DP engines, >= 1 */
+    int32_t E;    /* experts per layer, 1..1024 */
+    int32_t G;    /* EP ranks, 1..64 */
+    double alpha, beta, gamma;  /* score weights */
+    double m_uniform;           /* M_{e,g} everywhere when M is NULL */
+} moe_place_dims;
+
+/*
+ * Row length of moe_place_experts' rank_experts output: the largest number of
+ * experts one rank can hold, max_g min(cap[g], E) (0 for NULL arguments or
+ * E, G < 1).  Host only, no HIP call.
+ */
+size_t moe_place_slots(const moe_place_dims *dims, const int32_t *cap);
+
+/*
+ * New expert placement for L layers, one workgroup per layer.
+ *   cap           [G] int32 HOST array: experts rank g can host per layer,
+ *                 >= 0, with sum_g min(cap[g], E) >= E (else MOE_ERR_DIMS).
+ *   A             [L][S][E] int64: the window's source x expert counts (the
+ *                 per-layer `counts` of moe_route_stats, stacked).
+ *   B             [L][E] int64, nullable: aggregate loads; NULL = the column
+ *                 sums of A.
+ *   D             [S][G] fp64: communication cost from source s to rank g.
+ *   M             [L][E][G] fp64, nullable: cost of moving expert e to rank
+ *                 g; NULL = dims->m_uniform everywhere.
+ *   x0            [L][E] int32: rank hosting each expert now; a value outside
+ *                 [0, G) means the expert is hosted nowhere yet.
+ *   x             [L][E] int32 out: the new rank of each expert.
+ *   rank_experts  [L][G][slots] int32 out, nullable: the experts of each rank
+ *                 in ascending id order, padded with -1 (slots =
+ *                 moe_place_slots); the first entries of a row are the
+ *                 local_experts list moe_forward takes on that rank.
+ *   cost          [L][3] fp64 out, nullable: C_comm, C_load, C_mig of the new
+ *                 placement (sums in an unspecified order).
+ * Limits (MOE_ERR_UNSUPPORTED beyond them): E <= 1024, G <= 64, S*G <= 4096.
+ * int64 and fp64 arrays must be 8-byte aligned, int32 arrays 4-byte aligned
+ * (MOE_ERR_ALIGN).  Counts are converted to fp64 for the scores (exact below
+ * 2^53).  L = 0 is a no-op.
+ */
+int moe_place_experts(const moe_place_dims *dims, const int32_t *cap,
+                      const int64_t *A, const int64_t *B, const double *D,
+                      const double *M, const int32_t *x0, int32_t *x,
+                      int32_t *rank_experts, double *cost, void *stream);
 
 #ifdef __cplusplus
 }

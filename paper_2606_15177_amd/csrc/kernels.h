@@ -94,4 +94,27 @@ hipError_t launch_combine(int T, int k, int H, const uint16_t* y_perm, const int
                           const float* topk_w, const uint16_t* y_shared, uint16_t* out,
                           hipStream_t st);
 
+// ---- place.hip -------------------------------------------------------------
+// Source-aware expert placement, one workgroup per layer (see moe.h).
+constexpr int kPlaceMaxExperts = 1024;
+constexpr int kPlaceMaxRanks = 64;           // ranks are the lanes of one wave
+constexpr int kPlaceMaxSourceRanks = 4096;   // S*G entries of D staged in LDS
+constexpr int kPlaceMaxLdsBytes = 160 * 1024;
+struct PlaceArgs {
+  int L, S, E, G;
+  int slots;  // row length of rank_experts
+  double alpha, beta, gamma, m_uniform;
+  const int32_t* cap;  // host [G]
+  const int64_t* A;    // [L][S][E]
+  const int64_t* B;    // [L][E] or null
+  const double* D;     // [S][G]
+  const double* M;     // [L][E][G] or null
+  const int32_t* x0;   // [L][E]
+  int32_t* x;          // [L][E]
+  int32_t* rank_experts;  // [L][G][slots] or null
+  double* cost;           // [L][3] or null
+};
+size_t place_lds_bytes(int S, int E, int G);
+hipError_t launch_place(const PlaceArgs& a, hipStream_t st);
+
 }  // namespace moe

@@ -200,7 +200,7 @@ const char* moe_strerror(int s) {
     case MOE_ERR_UNSUPPORTED: return "dimensions beyond the kernels' limits";
     case MOE_ERR_WORKSPACE: return "workspace missing or too small";
     case MOE_ERR_DEVICE: return "kernel launch failed";
-    case MOE_ERR_ALIGN: return "pointer not 16-byte aligned";
+    case MOE_ERR_ALIGN: return "pointer not aligned as required";
     default: return "unknown status";
   }
 }
@@ -346,6 +346,57 @@ int moe_forward(const moe_dims* d, const float* logits, const int32_t* src, cons
   if (e != hipSuccess) return MOE_ERR_DEVICE;
   record(taps, 2 * MOE_STAGE_COMBINE + 1, st);
   return MOE_OK;
+}
+
+size_t moe_place_slots(const moe_place_dims* pd, const int32_t* cap) {
+  if (pd == nullptr || cap == nullptr || pd->E < 1 || pd->G < 1) return 0;
+  int slots = 0;
+  for (int g = 0; g < pd->G; ++g) slots = std::max(slots, std::min(std::max(cap[g], 0), pd->E));
+  return static_cast<size_t>(slots);
+}
+
+int moe_place_experts(const moe_place_dims* pd, const int32_t* cap, const int64_t* A,
+                      const int64_t* B, const double* D, const double* M, const int32_t* x0,
+                      int32_t* x, int32_t* rank_experts, double* cost, void* stream) {
+  if (pd == nullptr || cap == nullptr) return MOE_ERR_NULL;
+  if (pd->L < 0 || pd->S < 1 || pd->E < 1 || pd->G < 1) return MOE_ERR_DIMS;
+  if (pd->E > moe::kPlaceMaxExperts || pd->G > moe::kPlaceMaxRanks ||
+      static_cast<int64_t>(pd->S) * pd->G > moe::kPlaceMaxSourceRanks ||
+      moe::place_lds_bytes(pd->S, pd->E, pd->G) > static_cast<size_t>(moe::kPlaceMaxLdsBytes))
+    return MOE_ERR_UNSUPPORTED;
+  int64_t room = 0;
+  for (int g = 0; g < pd->G; ++g) {
+    if (cap[g] < 0) return MOE_ERR_DIMS;
+    room += std::min(cap[g], pd->E);
+  }
+  if (room < pd->E) return MOE_ERR_DIMS;  // some expert would have no rank
+  if (static_cast<int64_t>(pd->L) * pd->S * pd->E > (int64_t{1} << 40)) return MOE_ERR_UNSUPPORTED;
+  if (pd->L == 0) return MOE_OK;
+  if (!A || !D || !x0 || !x) return MOE_ERR_NULL;
+  auto al = [](const void* p, uintptr_t n) { return (reinterpret_cast<uintptr_t>(p) & (n - 1)) == 0; };
+  if (!al(A, 8) || !al(B, 8) || !al(D, 8) || !al(M, 8) || !al(cost, 8) || !al(x0, 4) || !al(x, 4) ||
+      !al(rank_experts, 4))
+    return MOE_ERR_ALIGN;
+  moe::PlaceArgs a{};
+  a.L = pd->L;
+  a.S = pd->S;
+  a.E = pd->E;
+  a.G = pd->G;
+  a.slots = static_cast<int>(moe_place_slots(pd, cap));
+  a.alpha = pd->alpha;
+  a.beta = pd->beta;
+  a.gamma = pd->gamma;
+  a.m_uniform = pd->m_uniform;
+  a.cap = cap;
+  a.A = A;
+  a.B = B;
+  a.D = D;
+  a.M = M;
+  a.x0 = x0;
+  a.x = x;
+  a.rank_experts = rank_experts;
+  a.cost = cost;
+  return status(moe::launch_place(a, static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

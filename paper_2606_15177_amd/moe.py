@@ -38,6 +38,12 @@ class MoeTaps(C.Structure):
                 ("events", C.c_void_p * (2 * len(STAGES)))]
 
 
+class MoePlaceDims(C.Structure):
+    _fields_ = [("L", C.c_int32), ("S", C.c_int32), ("E", C.c_int32), ("G", C.c_int32),
+                ("alpha", C.c_double), ("beta", C.c_double), ("gamma", C.c_double),
+                ("m_uniform", C.c_double)]
+
+
 class MoeError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
@@ -62,6 +68,8 @@ def _load() -> C.CDLL:
         "moe_combine": ([dp, vp, vp, vp, vp, vp, vp], i32),
         "moe_forward": ([dp, vp, vp, vp, vp, C.POINTER(MoeWeights), vp, vp, C.POINTER(MoeTaps),
                          vp, sz, vp], i32),
+        "moe_place_slots": ([C.POINTER(MoePlaceDims), vp], sz),
+        "moe_place_experts": ([C.POINTER(MoePlaceDims), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp], i32),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -125,6 +133,7 @@ _BF16 = (torch.bfloat16, torch.int16, torch.uint16)
 _I32 = (torch.int32,)
 _I64 = (torch.int64,)
 _F32 = (torch.float32,)
+_F64 = (torch.float64,)
 
 
 def _stream(stream) -> int | None:
@@ -191,6 +200,35 @@ def forward(d, logits, src, x, local_experts, weights, counts, out, ws, taps=Non
                             _ptr(out, _BF16), None if taps is None else C.byref(taps), _ptr(ws),
                             0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)),
            "moe_forward")
+
+
+PAPER_PLACE_WEIGHTS = (1.0, 0.0025, 1.0)  # (alpha, beta, gamma), Sec. 6
+
+
+def place_dims(L, S, E, G, alpha=1.0, beta=0.0025, gamma=1.0, m_uniform=1.0) -> MoePlaceDims:
+    return MoePlaceDims(L, S, E, G, alpha, beta, gamma, m_uniform)
+
+
+def _host_i32(a):
+    import numpy as np
+    a = np.ascontiguousarray(a.cpu().numpy() if isinstance(a, torch.Tensor) else a, dtype=np.int32)
+    return a, a.ctypes.data_as(C.c_void_p)
+
+
+def place_slots(pd: MoePlaceDims, cap) -> int:
+    cap_h, cap_p = _host_i32(cap)
+    return int(_lib.moe_place_slots(C.byref(pd), cap_p))
+
+
+def place_experts(pd: MoePlaceDims, cap, A, D, x0, x, B=None, M=None, rank_experts=None, cost=None,
+                  stream=None):
+    """moe_place_experts: cap is a host sequence of G ints, every tensor lives
+    on the GPU (A int64 [L,S,E], D fp64 [S,G], x0/x int32 [L,E], B int64 [L,E],
+    M fp64 [L,E,G], rank_experts int32 [L,G,slots], cost fp64 [L,3])."""
+    cap_h, cap_p = _host_i32(cap)
+    _check(_lib.moe_place_experts(C.byref(pd), cap_p, _ptr(A, _I64), _ptr(B, _I64), _ptr(D, _F64),
+                                  _ptr(M, _F64), _ptr(x0, _I32), _ptr(x, _I32), _ptr(rank_experts, _I32),
+                                  _ptr(cost, _F64), _stream(stream)), "moe_place_experts")
 
 
 class MoeLayer:

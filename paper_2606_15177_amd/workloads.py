@@ -26,6 +26,7 @@ _TAG = {
     "src": 1, "logits": 2, "bias": 3, "local": 4, "x": 5,
     "w_gate": 6, "w_up": 7, "w_down": 8,
     "sh_gate": 9, "sh_up": 10, "sh_down": 11,
+    "place_counts": 12, "place_bias": 13, "place_x0": 14, "place_m": 15,
 }
 
 WEIGHT_STD = 0.02
@@ -234,3 +235,87 @@ def make_workload(cfg: MoeConfig, seed: int = 0, weights: bool = True) -> dict:
     if weights:
         w.update(make_weights(cfg, seed))
     return w
+
+
+# ---------------------------------------------------------------------------
+# Inputs of source-aware expert placement: the statistics of one profiling
+# window (Sec. 5.1) for every MoE layer of a model, the source/rank cost
+# matrix, the current placement and the capacities.
+
+
+@dataclasses.dataclass(frozen=True)
+class PlaceConfig:
+    """Shape and input recipe of one placement problem."""
+    name: str
+    L: int                  # MoE layers placed together
+    S: int                  # source DP engines
+    E: int                  # experts per layer
+    G: int                  # EP ranks
+    k: int                  # experts per token
+    tokens_per_source: int  # tokens each source routes through a layer per window
+    zipf_s: float = 1.0     # per-source Zipf popularity (its own ranking per source and layer)
+    hot_per_source: int = 0  # extra affinity of each source for its own expert set
+    hot_bias: float = 0.0
+    m_uniform: float = 64.0  # migration cost per changed indicator, in token units
+    x0_layout: str = "contiguous"  # contiguous (rank g hosts experts [g E/G, (g+1) E/G)) | random
+
+    @property
+    def cap(self) -> np.ndarray:
+        return np.full(self.G, -(-self.E // self.G), dtype=np.int32)
+
+
+# A small case, the Qwen3-30B-A3B deployment of the paper's evaluation (48 MoE
+# layers of 128 experts, DP8 attention feeding EP8, Sec. 7.1), a
+# DeepSeek-V3-shaped model on EP8 (58 MoE layers of 256 experts) and the same
+# model spread over 64 ranks with 64 sources (the largest D the kernel stages).
+PLACE_CONFIGS: dict[str, PlaceConfig] = {
+    "place_tiny": PlaceConfig("place_tiny", L=3, S=4, E=16, G=4, k=2, tokens_per_source=256,
+                              hot_per_source=2, hot_bias=1.5, x0_layout="random"),
+    "place_qwen3_30b_a3b": PlaceConfig("place_qwen3_30b_a3b", L=48, S=8, E=128, G=8, k=8,
+                                       tokens_per_source=4096, zipf_s=1.0, hot_per_source=8,
+                                       hot_bias=2.0),
+    "place_dsv3_ep8": PlaceConfig("place_dsv3_ep8", L=58, S=8, E=256, G=8, k=8,
+                                  tokens_per_source=4096, zipf_s=1.2),
+    "place_dsv3_ep64": PlaceConfig("place_dsv3_ep64", L=58, S=64, E=256, G=64, k=8,
+                                   tokens_per_source=512, zipf_s=1.2, x0_layout="random"),
+}
+
+
+def make_place_inputs(cfg: PlaceConfig, seed: int = 0) -> dict:
+    """A [L,S,E] int64 window counts, D [S,G] fp64, x0 [L,E] int32, cap [G].
+
+    Source s of layer l routes tokens_per_source * k pairs, multinomially over
+    experts with probabilities proportional to exp(bias), where the bias is a
+    per-source Zipf(zipf_s) log-popularity over its own random ranking plus
+    hot_bias on hot_per_source experts of its own.  Source s sits with rank
+    s * G // S: reaching that rank costs 0, any other 1.  M is uniform
+    (m_uniform), so it is not drawn."""
+    L, S, E, G = cfg.L, cfg.S, cfg.E, cfg.G
+    brng = _rng(seed, "place_bias")
+    crng = _rng(seed, "place_counts")
+    A = np.empty((L, S, E), dtype=np.int64)
+    for l in range(L):
+        for s in range(S):
+            bias = _zipf_log_bias(brng, E, cfg.zipf_s).astype(np.float64)
+            if cfg.hot_per_source:
+                bias[brng.choice(E, cfg.hot_per_source, replace=False)] += cfg.hot_bias
+            p = np.exp(bias - bias.max())
+            A[l, s] = crng.multinomial(cfg.tokens_per_source * cfg.k, p / p.sum())
+    home = np.arange(S) * G // S
+    D = np.ones((S, G), dtype=np.float64)
+    D[np.arange(S), home] = 0.0
+    if cfg.x0_layout == "contiguous":
+        x0 = np.tile((np.arange(E) * G // E).astype(np.int32), (L, 1))
+    elif cfg.x0_layout == "random":
+        xr = _rng(seed, "place_x0")
+        x0 = np.stack([np.repeat(np.arange(G, dtype=np.int32), -(-E // G))[:E][xr.permutation(E)]
+                       for _ in range(L)])
+    else:
+        raise ValueError(cfg.x0_layout)
+    return dict(A=A, D=D, x0=np.ascontiguousarray(x0, dtype=np.int32), cap=cfg.cap,
+                m_uniform=cfg.m_uniform)
+
+
+def make_migration_costs(L: int, E: int, G: int, seed: int = 0, scale: float = 64.0) -> np.ndarray:
+    """A non-uniform M [L,E,G] fp64 in [0, scale), for tests of the M input."""
+    return _rng(seed, "place_m").uniform(0.0, scale, size=(L, E, G))

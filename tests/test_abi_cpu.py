@@ -105,3 +105,53 @@ def test_entry_points_reject_before_launch(moe):
                            None) == moe.MOE_ERR_WORKSPACE
     assert lib.moe_forward(C.byref(d8), 16, 16, 16, None, C.byref(w), 16, 16, None, 128, ws_need,
                            None) == moe.MOE_ERR_ALIGN      # workspace not 256-byte aligned
+
+
+# ------------------------------------------------------------ placement ----
+
+def _cap(vals):
+    import numpy as np
+    a = np.ascontiguousarray(vals, dtype=np.int32)
+    return a, a.ctypes.data_as(C.c_void_p)
+
+
+def test_place_slots(moe):
+    lib = moe._lib
+    pd = moe.place_dims(L=2, S=2, E=10, G=3)
+    assert moe.place_slots(pd, [4, 4, 4]) == 4
+    assert moe.place_slots(pd, [0, 25, 3]) == 10      # a rank never holds more than E
+    assert moe.place_slots(pd, [-3, 5, 5]) == 5
+    assert lib.moe_place_slots(None, None) == 0
+
+
+@pytest.mark.parametrize("change,cap,code", [
+    (dict(), [4, 4], -1),                    # A missing (see below: all pointers NULL)
+    (dict(L=-1), [4, 4], -2), (dict(S=0), [4, 4], -2), (dict(E=0), [4, 4], -2),
+    (dict(G=0), [], -2),
+    (dict(), [4, 3], -2),                    # 7 places for 8 experts
+    (dict(), [-1, 9], -2),                   # negative capacity
+    (dict(E=1025), [1025, 1025], -3), (dict(G=65), [1] * 65, -3),
+    (dict(S=2049), [8, 8], -3),              # S*G > 4096
+])
+def test_place_rejects_before_launch(moe, change, cap, code):
+    base = dict(L=2, S=2, E=8, G=2)
+    base.update(change)
+    pd = moe.place_dims(**base)
+    cap_a, cap_p = _cap(cap)
+    rc = moe._lib.moe_place_experts(C.byref(pd), cap_p, None, None, None, None, None, None, None, None, None)
+    assert rc == code
+
+
+def test_place_checks_alignment_and_noop(moe):
+    lib = moe._lib
+    pd = moe.place_dims(L=2, S=2, E=8, G=2)
+    cap_a, cap_p = _cap([4, 4])
+    assert lib.moe_place_experts(None, cap_p, 16, None, 16, None, 16, 16, None, None, None) == moe.MOE_ERR_NULL
+    assert lib.moe_place_experts(C.byref(pd), None, 16, None, 16, None, 16, 16, None, None, None) == moe.MOE_ERR_NULL
+    assert lib.moe_place_experts(C.byref(pd), cap_p, 12, None, 16, None, 16, 16, None, None, None) == moe.MOE_ERR_ALIGN
+    assert lib.moe_place_experts(C.byref(pd), cap_p, 16, None, 16, 20, 16, 16, None, None, None) == moe.MOE_ERR_ALIGN
+    assert lib.moe_place_experts(C.byref(pd), cap_p, 16, None, 16, None, 18, 16, None, None, None) == moe.MOE_ERR_ALIGN
+    # L = 0: nothing to place, nothing launched, no pointer needed
+    pd0 = moe.place_dims(L=0, S=2, E=8, G=2)
+    assert lib.moe_place_experts(C.byref(pd0), cap_p, None, None, None, None, None, None, None, None,
+                                 None) == moe.MOE_OK
