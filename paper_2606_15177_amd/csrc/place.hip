@@ -32,7 +32,6 @@ namespace {
 
 constexpr int kPlaceThreads = 256;
 constexpr int kPlaceWaves = kPlaceThreads / kWave;
-constexpr int kChunkTerms = 2048;  // (expert, rank) term pairs staged per chunk
 
 struct PlaceKernelArgs {
   const int64_t* A;
@@ -48,52 +47,202 @@ struct PlaceKernelArgs {
   int cap[kPlaceMaxRanks];
 };
 
+typedef int64_t i64x2 __attribute__((ext_vector_type(2)));
+
 struct PlaceLds {
-  int64_t* B;      // [E] aggregate load
-  int64_t* V;      // [E] source-aware volume
+  i64x2* bv;       // [E] (B, V) of each expert: aggregate load, source-aware volume
   double* D;       // [S*G]
   double2* terms;  // [chunk*G] (C^comm, C^mig) of the staged chunk
-  double2* won;    // [E] (C^comm, C^mig) at the chosen rank
   int64_t* bo;     // [E] B of the expert in hotness position i
   int32_t* order;  // [E] expert in hotness position i
-  int32_t* home;   // [E] x^0 by expert
-  int32_t* xs;     // [E] chosen rank by expert
+  int32_t* ho;     // [E] x^0 of the expert in hotness position i
+  int32_t* xpos;   // [E] rank chosen for hotness position i
+  int32_t* xs;     // [E] rank chosen for each expert
   int32_t* fill;   // [kPlaceMaxRanks] experts placed per rank
-  int64_t* red_i;  // [kPlaceWaves]
-  double* red_d;   // [3 * kPlaceWaves]
+  int64_t* red_i;  // [2 * kPlaceWaves]
+  double* red_d;   // [2 * kPlaceWaves]
+  int64_t* A;      // [S*E] this layer's counts when they fit (a_staged), else
+                   // [chunk][S] the columns of the staged chunk's experts
 };
+
+// The layer's A is staged in LDS when it takes at most this many bytes;
+// otherwise each chunk stages its experts' columns, at most as many bytes.
+constexpr size_t kStageABytes = 32 * 1024;
+__host__ __device__ inline bool a_staged(int S, int E) {
+  return static_cast<size_t>(S) * E * sizeof(int64_t) <= kStageABytes;
+}
+
+// Experts per staged chunk: at most 2048 (expert, rank) terms, and when A is
+// not staged whole, at most kStageABytes of A columns.
+__host__ __device__ inline int place_chunk_experts(int S, int E, int G) {
+  int c = 2048 / G;
+  if (!a_staged(S, E)) c = c < static_cast<int>(kStageABytes / (8 * S)) ? c : static_cast<int>(kStageABytes / (8 * S));
+  c = c < E ? c : E;
+  return c > 1 ? c : 1;
+}
 
 __host__ __device__ inline size_t align16(size_t v) { return (v + 15) & ~static_cast<size_t>(15); }
 
 // Byte offsets of the LDS carve; the same function sizes the launch.
 __host__ __device__ inline size_t place_lds_layout(int S, int E, int G, int chunk, size_t* off) {
   size_t o = 0;
-  off[0] = o; o = align16(o + sizeof(int64_t) * E);               // B
-  off[1] = o; o = align16(o + sizeof(int64_t) * E);               // V
-  off[2] = o; o = align16(o + sizeof(double) * S * G);            // D
-  off[3] = o; o = align16(o + sizeof(double2) * chunk * G);       // terms
-  off[4] = o; o = align16(o + sizeof(double2) * E);               // won
-  off[5] = o; o = align16(o + sizeof(int64_t) * E);               // bo
-  off[6] = o; o = align16(o + sizeof(int32_t) * E);               // order
-  off[7] = o; o = align16(o + sizeof(int32_t) * E);               // home
-  off[8] = o; o = align16(o + sizeof(int32_t) * E);               // xs
-  off[9] = o; o = align16(o + sizeof(int32_t) * kPlaceMaxRanks);  // fill
-  off[10] = o; o = align16(o + sizeof(int64_t) * kPlaceWaves);    // red_i
-  off[11] = o; o = align16(o + sizeof(double) * 3 * kPlaceWaves); // red_d
+  off[0] = o; o = align16(o + 16 * static_cast<size_t>(E));                 // bv
+  off[1] = o; o = align16(o + sizeof(double) * S * G);                      // D
+  off[2] = o; o = align16(o + sizeof(double2) * chunk * G);                 // terms
+  off[3] = o; o = align16(o + sizeof(int64_t) * E);                         // bo
+  off[4] = o; o = align16(o + sizeof(int32_t) * E);                         // order
+  off[5] = o; o = align16(o + sizeof(int32_t) * E);                         // ho
+  off[6] = o; o = align16(o + sizeof(int32_t) * E);                         // xpos
+  off[7] = o; o = align16(o + sizeof(int32_t) * E);                         // xs
+  off[8] = o; o = align16(o + sizeof(int32_t) * kPlaceMaxRanks);            // fill
+  off[9] = o; o = align16(o + sizeof(int64_t) * 2 * kPlaceWaves);           // red_i
+  off[10] = o; o = align16(o + sizeof(double) * 2 * kPlaceWaves);           // red_d
+  off[11] = o;
+  o = align16(o + sizeof(int64_t) * S * (a_staged(S, E) ? E : chunk));       // A or its columns
   return o;
 }
+constexpr int kLdsParts = 12;
 
 __device__ __forceinline__ double mig_cost(const PlaceKernelArgs& a, int l, int e, int g) {
   return a.M ? a.M[(static_cast<size_t>(l) * a.E + e) * a.G + g] : a.m_uniform;
 }
 
-// Candidate (score, key) a beats b.  key: bit 31 = rank full, bit 30 = not
-// the expert's current rank, bits 6..16 = experts placed, bits 0..5 = rank.
-__device__ __forceinline__ bool beats(double as, uint32_t ak, double bs, uint32_t bk) {
-  const uint32_t a_full = ak >> 31, b_full = bk >> 31;
-  if (a_full != b_full) return a_full < b_full;
-  if (as != bs) return as < bs;
-  return (ak & 0x7fffffffu) < (bk & 0x7fffffffu);
+// C^mig of expert e on rank g: zero on its current rank, else the two
+// indicator changes M_{e,g} and (when it has a rank) M_{e,home}.
+__device__ __forceinline__ double mig_term(const PlaceKernelArgs& a, int l, int e, int g, int home) {
+  const bool home_ok = home >= 0 && home < a.G;
+  if (home_ok && g == home) return 0.0;
+  double m = mig_cost(a, l, e, g);
+  if (home_ok) m = m + mig_cost(a, l, e, home);
+  return m;
+}
+
+// C^comm of an expert on rank g: sum_s A_{s,e} D_{s,g}, in s order, with
+// A_{s,e} = col[s * stride] (the layer's A in LDS, or its staged column);
+// eight loads are issued before their products are summed.
+__device__ __forceinline__ double comm_term(const int64_t* col, int stride, const double* D, int S, int G,
+                                            int g) {
+  double comm = 0.0;
+  int src = 0;
+  for (; src + 8 <= S; src += 8) {
+    int64_t av[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) av[j] = col[(src + j) * stride];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) comm = comm + static_cast<double>(av[j]) * D[(src + j) * G + g];
+  }
+  for (; src < S; ++src) comm = comm + static_cast<double>(col[src * stride]) * D[src * G + g];
+  return comm;
+}
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+  return static_cast<uint32_t>(
+      __builtin_amdgcn_update_dpp(static_cast<int>(v), static_cast<int>(v), CTRL, 0xf, 0xf, false));
+}
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
+  const int lo = __builtin_amdgcn_update_dpp(__double2loint(v), __double2loint(v), CTRL, 0xf, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp(__double2hiint(v), __double2hiint(v), CTRL, 0xf, 0xf, false);
+  return __hiloint2double(hi, lo);
+}
+// Scores are never NaN here (a NaN score is replaced by +inf first), so the
+// hardware minimum is exact; of -0.0 and +0.0 it may return either, which the
+// equality test of the tie phase treats alike.
+__device__ __forceinline__ double min_f64(double a, double b) { return __builtin_fmin(a, b); }
+__device__ __forceinline__ uint32_t min_u32(uint32_t a, uint32_t b) { return b < a ? b : a; }
+
+// DPP controls: swap neighbours, swap pairs, mirror each half row (lane i <->
+// 7 - i), mirror each row (lane i <-> 15 - i).  After the four levels every
+// lane of a 16-lane row holds the row's minimum.
+constexpr int kDppSwap1 = 0xB1;   // quad_perm [1, 0, 3, 2]
+constexpr int kDppSwap2 = 0x4E;   // quad_perm [2, 3, 0, 1]
+constexpr int kDppHalfMirror = 0x141;
+constexpr int kDppMirror = 0x140;
+
+// Minimum over the first 2^LEVELS lanes (every lane among them gets it;
+// lanes past G must hold values that do not win).
+template <int LEVELS>
+__device__ __forceinline__ double lanes_min_f64(double v) {
+  if constexpr (LEVELS > 0) v = min_f64(v, dpp_f64<kDppSwap1>(v));
+  if constexpr (LEVELS > 1) v = min_f64(v, dpp_f64<kDppSwap2>(v));
+  if constexpr (LEVELS > 2) v = min_f64(v, dpp_f64<kDppHalfMirror>(v));
+  if constexpr (LEVELS > 3) v = min_f64(v, dpp_f64<kDppMirror>(v));
+  if constexpr (LEVELS > 4) v = min_f64(v, __shfl_xor(v, 16));
+  if constexpr (LEVELS > 5) v = min_f64(v, __shfl_xor(v, 32));
+  return v;
+}
+template <int LEVELS>
+__device__ __forceinline__ uint32_t lanes_min_u32(uint32_t v) {
+  if constexpr (LEVELS > 0) v = min_u32(v, dpp_u32<kDppSwap1>(v));
+  if constexpr (LEVELS > 1) v = min_u32(v, dpp_u32<kDppSwap2>(v));
+  if constexpr (LEVELS > 2) v = min_u32(v, dpp_u32<kDppHalfMirror>(v));
+  if constexpr (LEVELS > 3) v = min_u32(v, dpp_u32<kDppMirror>(v));
+  if constexpr (LEVELS > 4) v = min_u32(v, __shfl_xor(v, 16));
+  if constexpr (LEVELS > 5) v = min_u32(v, __shfl_xor(v, 32));
+  return v;
+}
+
+// State of rank g, held by lane g of wave 0: experts placed, load placed (as
+// int64, and as an exact double in FAST mode), u2 = (L_g - Lbar)^2, and the
+// C^comm and C^mig of the experts it won.
+struct RankState {
+  int placed;
+  int64_t load;
+  double loadd, u2, comm, mig;
+};
+
+// Wave 0's greedy over one staged chunk of nc hotness positions from c0.
+// FAST requires every partial load to be an integer below 2^53, so that
+// (double)(L + B) equals the double sum of the two exact conversions.
+template <bool FAST, int LEVELS>
+__device__ __forceinline__ void place_chunk_steps(const PlaceKernelArgs& a, const PlaceLds& s, int c0, int nc,
+                                                  double mean, int lane, int cap_g, RankState& r) {
+  const int G = a.G;
+  const int gl = lane < G ? lane : G - 1;   // lanes past G read a valid term and stay closed
+  double2 t_next = s.terms[gl];
+  int64_t be_next = s.bo[c0];
+  int home_next = s.ho[c0];
+  int xw = 0;   // lane j keeps the rank of step j of the current 64
+  for (int i = 0; i < nc; ++i) {
+    const double2 t = t_next;
+    const int64_t be = be_next;
+    const int home = home_next;
+    const int in = min(i + 1, nc - 1);
+    t_next = s.terms[in * G + gl];
+    be_next = s.bo[c0 + in];
+    home_next = s.ho[c0 + in];
+
+    const bool open = r.placed < cap_g;
+    const double bd = static_cast<double>(be);
+    const double v = (FAST ? r.loadd + bd : static_cast<double>(r.load + be)) - mean;
+    const double vv = v * v;
+    const double c_load = vv - r.u2;
+    double score = a.alpha * t.x;
+    score = score + a.beta * c_load;
+    score = score + a.gamma * t.y;
+    score = (open & (score == score)) ? score : __builtin_inf();
+    // ties: a full rank loses, then the current rank wins, then fewer
+    // experts placed, then the lower rank
+    const uint32_t key = (open ? 0u : 0x80000000u) | (lane == home ? 0u : 0x40000000u) |
+                         (static_cast<uint32_t>(r.placed) << 6) | static_cast<uint32_t>(lane);
+    const double best = lanes_min_f64<LEVELS>(score);
+    const uint32_t k = lanes_min_u32<LEVELS>(score == best ? key : 0xffffffffu);
+    const int w = static_cast<int>(__builtin_amdgcn_readfirstlane(k) & 63u);
+    const bool won = lane == w;
+    r.placed += won ? 1 : 0;
+    if (FAST)
+      r.loadd = won ? r.loadd + bd : r.loadd;
+    else
+      r.load += won ? be : 0;
+    r.u2 = won ? vv : r.u2;   // the new load's (L - Lbar) is this step's v
+    r.comm = won ? r.comm + t.x : r.comm;
+    r.mig = won ? r.mig + t.y : r.mig;
+    xw = lane == (i & 63) ? w : xw;
+    if ((i & 63) == 63 || i == nc - 1) {
+      if (lane <= (i & 63)) s.xpos[c0 + (i & ~63) + lane] = xw;
+    }
+  }
 }
 
 __device__ __forceinline__ int64_t wave_sum_i64(int64_t v) {
@@ -114,140 +263,155 @@ __global__ __launch_bounds__(kPlaceThreads) void place_kernel(PlaceKernelArgs a)
   const int wave = tid / kWave;
   const int S = a.S, E = a.E, G = a.G;
   const int64_t* A_l = a.A + static_cast<size_t>(l) * S * E;
+  const int32_t* x0_l = a.x0 + static_cast<size_t>(l) * E;
 
-  size_t off[12];
+  size_t off[kLdsParts];
   place_lds_layout(S, E, G, a.chunk, off);
   PlaceLds s;
-  s.B = reinterpret_cast<int64_t*>(place_smem + off[0]);
-  s.V = reinterpret_cast<int64_t*>(place_smem + off[1]);
-  s.D = reinterpret_cast<double*>(place_smem + off[2]);
-  s.terms = reinterpret_cast<double2*>(place_smem + off[3]);
-  s.won = reinterpret_cast<double2*>(place_smem + off[4]);
-  s.bo = reinterpret_cast<int64_t*>(place_smem + off[5]);
-  s.order = reinterpret_cast<int32_t*>(place_smem + off[6]);
-  s.home = reinterpret_cast<int32_t*>(place_smem + off[7]);
-  s.xs = reinterpret_cast<int32_t*>(place_smem + off[8]);
-  s.fill = reinterpret_cast<int32_t*>(place_smem + off[9]);
-  s.red_i = reinterpret_cast<int64_t*>(place_smem + off[10]);
-  s.red_d = reinterpret_cast<double*>(place_smem + off[11]);
+  s.bv = reinterpret_cast<i64x2*>(place_smem + off[0]);
+  s.D = reinterpret_cast<double*>(place_smem + off[1]);
+  s.terms = reinterpret_cast<double2*>(place_smem + off[2]);
+  s.bo = reinterpret_cast<int64_t*>(place_smem + off[3]);
+  s.order = reinterpret_cast<int32_t*>(place_smem + off[4]);
+  s.ho = reinterpret_cast<int32_t*>(place_smem + off[5]);
+  s.xpos = reinterpret_cast<int32_t*>(place_smem + off[6]);
+  s.xs = reinterpret_cast<int32_t*>(place_smem + off[7]);
+  s.fill = reinterpret_cast<int32_t*>(place_smem + off[8]);
+  s.red_i = reinterpret_cast<int64_t*>(place_smem + off[9]);
+  s.red_d = reinterpret_cast<double*>(place_smem + off[10]);
+  const bool staged = a_staged(S, E);
+  s.A = reinterpret_cast<int64_t*>(place_smem + off[11]);
 
-  // 1. hotness signals, current ranks, D
+  // 1. hotness signals, D, and the layer's A when it fits in LDS
   int64_t part = 0;
+  int negative = 0;
   for (int e = tid; e < E; e += kPlaceThreads) {
     int64_t v = 0;
-    for (int src = 0; src < S; ++src) v += A_l[static_cast<size_t>(src) * E + e];
+#pragma unroll 8
+    for (int src = 0; src < S; ++src) {
+      const int64_t c = A_l[static_cast<size_t>(src) * E + e];
+      if (staged) s.A[src * E + e] = c;
+      v += c;
+    }
     const int64_t b = a.B ? a.B[static_cast<size_t>(l) * E + e] : v;
-    s.V[e] = v;
-    s.B[e] = b;
-    s.home[e] = a.x0[static_cast<size_t>(l) * E + e];
+    i64x2 bv;
+    bv.x = b;
+    bv.y = v;
+    s.bv[e] = bv;
     part += b;
+    negative |= static_cast<int>(b < 0);
   }
   for (int i = tid; i < S * G; i += kPlaceThreads) s.D[i] = a.D[i];
   part = wave_sum_i64(part);
-  if (lane == 0) s.red_i[wave] = part;
+  const int64_t neg_w = wave_sum_i64(negative);
+  if (lane == 0) {
+    s.red_i[wave] = part;
+    s.red_i[kPlaceWaves + wave] = neg_w;
+  }
   __syncthreads();
-  int64_t total = 0;
-  for (int w = 0; w < kPlaceWaves; ++w) total += s.red_i[w];
+  int64_t total = 0, n_negative = 0;
+  for (int w = 0; w < kPlaceWaves; ++w) {
+    total += s.red_i[w];
+    n_negative += s.red_i[kPlaceWaves + w];
+  }
   // every expert is placed, so the final average rank load is known up front
   const double mean = static_cast<double>(total) / G;
+  // non-negative loads whose total is below 2^53: every partial load is an
+  // exactly representable integer
+  const bool fast = n_negative == 0 && total < (int64_t{1} << 53);
 
-  // 2. hotness order: position = number of experts that come first
-  for (int e = tid; e < E; e += kPlaceThreads) {
-    const int64_t be = s.B[e], ve = s.V[e];
-    int pos = 0;
-    for (int f = 0; f < E; ++f) {
-      const int64_t bf = s.B[f], vf = s.V[f];
-      pos += (bf > be) || (bf == be && (vf > ve || (vf == ve && f < e)));
+  // 2. hotness order: an expert's position is the number of experts ahead of
+  // it; tpe consecutive lanes split the count of one expert
+  int tpe = 1;
+  while (tpe < kWave && tpe * 2 * E <= kPlaceThreads) tpe *= 2;
+  for (int idx = tid; idx < E * tpe; idx += kPlaceThreads) {
+    const int e = idx / tpe;
+    const int sub = idx - e * tpe;
+    const i64x2 me = s.bv[e];
+    auto before = [&](const i64x2 o, int f) {
+      return static_cast<int>((o.x > me.x) | ((o.x == me.x) & ((o.y > me.y) | ((o.y == me.y) & (f < e)))));
+    };
+    int ahead = 0;
+    int f = sub;
+    for (; f + 3 * tpe < E; f += 4 * tpe) {   // four independent loads per round
+      const i64x2 o0 = s.bv[f], o1 = s.bv[f + tpe], o2 = s.bv[f + 2 * tpe], o3 = s.bv[f + 3 * tpe];
+      ahead += before(o0, f) + before(o1, f + tpe) + before(o2, f + 2 * tpe) + before(o3, f + 3 * tpe);
     }
-    s.order[pos] = e;
-    s.bo[pos] = be;
+    for (; f < E; f += tpe) ahead += before(s.bv[f], f);
+    for (int m = tpe / 2; m > 0; m >>= 1) ahead += __shfl_xor(ahead, m);
+    if (sub == 0) {
+      s.order[ahead] = e;
+      s.bo[ahead] = me.x;
+      s.ho[ahead] = x0_l[e];
+    }
   }
   __syncthreads();
 
   // 3. greedy, hottest first; wave 0 lane g keeps rank g's state
-  int placed = 0;
-  int64_t load = 0;
+  RankState r{0, 0, 0.0, mean * mean, 0.0, 0.0};   // u2 = (0 - mean)^2
   const int cap_g = lane < G ? a.cap[lane] : 0;
-  int span = 1;
-  while (span < G) span <<= 1;
+  int levels = 0;   // butterfly levels that cover G lanes
+  while ((1 << levels) < G) ++levels;
   for (int c0 = 0; c0 < E; c0 += a.chunk) {
     const int nc = min(a.chunk, E - c0);
+    if (!staged) {   // this chunk's columns of A, [i][S]
+      for (int q = tid; q < nc * S; q += kPlaceThreads) {
+        const int i = q / S;
+        const int src = q - i * S;
+        s.A[q] = A_l[static_cast<size_t>(src) * E + s.order[c0 + i]];
+      }
+      __syncthreads();
+    }
     for (int p = tid; p < nc * G; p += kPlaceThreads) {
       const int i = p / G;
       const int g = p - i * G;
       const int e = s.order[c0 + i];
-      double comm = 0.0;
-      for (int src = 0; src < S; ++src)
-        comm = comm + static_cast<double>(A_l[static_cast<size_t>(src) * E + e]) * s.D[src * G + g];
-      const int home = s.home[e];
-      const bool home_ok = home >= 0 && home < G;
-      double mig = 0.0;
-      if (!(home_ok && g == home)) {
-        mig = mig_cost(a, l, e, g);
-        if (home_ok) mig = mig + mig_cost(a, l, e, home);
-      }
+      const double comm = staged ? comm_term(s.A + e, E, s.D, S, G, g) : comm_term(s.A + i * S, 1, s.D, S, G, g);
+      const double mig = mig_term(a, l, e, g, s.ho[c0 + i]);
       s.terms[p] = make_double2(comm, mig);
     }
     __syncthreads();
     if (wave == 0) {
-      for (int i = 0; i < nc; ++i) {
-        const int e = s.order[c0 + i];
-        const int64_t be = s.bo[c0 + i];
-        const int home = s.home[e];
-        const bool open = lane < G && placed < cap_g;
-        double score = __builtin_inf();
-        double2 t = make_double2(0.0, 0.0);
-        if (open) {
-          t = s.terms[i * G + lane];
-          const double u = static_cast<double>(load) - mean;
-          const double v = static_cast<double>(load + be) - mean;
-          const double c_load = v * v - u * u;
-          score = a.alpha * t.x;
-          score = score + a.beta * c_load;
-          score = score + a.gamma * t.y;
-          if (score != score) score = __builtin_inf();
-        }
-        uint32_t key = (open ? 0u : 0x80000000u) | (lane == home ? 0u : 0x40000000u) |
-                       (static_cast<uint32_t>(placed) << 6) | static_cast<uint32_t>(lane);
-        for (int o = 1; o < span; o <<= 1) {
-          const double os = __shfl_xor(score, o);
-          const uint32_t ok = __shfl_xor(key, o);
-          if (beats(os, ok, score, key)) {
-            score = os;
-            key = ok;
-          }
-        }
-        const int w = static_cast<int>(__builtin_amdgcn_readfirstlane(key) & 63u);
-        if (lane == w) {
-          placed += 1;
-          load += be;
-          s.xs[e] = w;
-          s.won[e] = t;
-        }
+      switch ((fast ? 8 : 0) + levels) {
+#define PLACE_STEPS(F, LV)                                              \
+  case (F ? 8 : 0) + LV:                                                \
+    place_chunk_steps<F, LV>(a, s, c0, nc, mean, lane, cap_g, r);      \
+    break;
+        PLACE_STEPS(true, 0) PLACE_STEPS(true, 1) PLACE_STEPS(true, 2) PLACE_STEPS(true, 3)
+        PLACE_STEPS(true, 4) PLACE_STEPS(true, 5) PLACE_STEPS(true, 6)
+        PLACE_STEPS(false, 0) PLACE_STEPS(false, 1) PLACE_STEPS(false, 2) PLACE_STEPS(false, 3)
+        PLACE_STEPS(false, 4) PLACE_STEPS(false, 5) PLACE_STEPS(false, 6)
+#undef PLACE_STEPS
+        default: break;
       }
     }
     __syncthreads();
   }
 
-  // 4. results
+  // 4. results: the objective's terms from the ranks' sums, the placement by
+  // expert, and each rank's experts in ascending order
+  for (int i = tid; i < E; i += kPlaceThreads) s.xs[s.order[i]] = s.xpos[i];
   if (wave == 0) {
-    if (lane < G) s.fill[lane] = placed;
+    if (lane < G) s.fill[lane] = r.placed;
     if (a.cost) {
-      const double d = lane < G ? static_cast<double>(load) - mean : 0.0;
-      const double c_load = wave_sum_f64(d * d);
-      if (lane == 0) a.cost[static_cast<size_t>(l) * 3 + 1] = c_load;
+      const bool rank = lane < G;
+      const double c_comm = wave_sum_f64(rank ? r.comm : 0.0);
+      const double c_load = wave_sum_f64(rank ? r.u2 : 0.0);
+      const double c_mig = wave_sum_f64(rank ? r.mig : 0.0);
+      if (lane == 0) {
+        a.cost[static_cast<size_t>(l) * 3 + 0] = c_comm;
+        a.cost[static_cast<size_t>(l) * 3 + 1] = c_load;
+        a.cost[static_cast<size_t>(l) * 3 + 2] = c_mig;
+      }
     }
   }
   __syncthreads();
-  double c_comm = 0.0, c_mig = 0.0;
   for (int e = tid; e < E; e += kPlaceThreads) {
     const int g = s.xs[e];
     a.x[static_cast<size_t>(l) * E + e] = g;
-    c_comm = c_comm + s.won[e].x;
-    c_mig = c_mig + s.won[e].y;
     if (a.rank_experts) {
       int pos = 0;
-      for (int f = 0; f < e; ++f) pos += s.xs[f] == g;
+      for (int f = 0; f < e; ++f) pos += static_cast<int>(s.xs[f] == g);
       a.rank_experts[(static_cast<size_t>(l) * G + g) * a.slots + pos] = e;
     }
   }
@@ -258,33 +422,13 @@ __global__ __launch_bounds__(kPlaceThreads) void place_kernel(PlaceKernelArgs a)
         a.rank_experts[static_cast<size_t>(l) * G * a.slots + i] = -1;
     }
   }
-  if (a.cost) {
-    c_comm = wave_sum_f64(c_comm);
-    c_mig = wave_sum_f64(c_mig);
-    if (lane == 0) {
-      s.red_d[wave] = c_comm;
-      s.red_d[kPlaceWaves + wave] = c_mig;
-    }
-    __syncthreads();
-    if (tid == 0) {
-      double sc = 0.0, sm = 0.0;
-      for (int w = 0; w < kPlaceWaves; ++w) {
-        sc = sc + s.red_d[w];
-        sm = sm + s.red_d[kPlaceWaves + w];
-      }
-      a.cost[static_cast<size_t>(l) * 3 + 0] = sc;
-      a.cost[static_cast<size_t>(l) * 3 + 2] = sm;
-    }
-  }
 }
 
 }  // namespace
 
-int place_chunk(int E, int G) { return min(E, max(1, kChunkTerms / G)); }
-
 size_t place_lds_bytes(int S, int E, int G) {
-  size_t off[12];
-  return place_lds_layout(S, E, G, place_chunk(E, G), off);
+  size_t off[kLdsParts];
+  return place_lds_layout(S, E, G, place_chunk_experts(S, E, G), off);
 }
 
 hipError_t launch_place(const PlaceArgs& h, hipStream_t st) {
@@ -306,7 +450,7 @@ hipError_t launch_place(const PlaceArgs& h, hipStream_t st) {
   a.E = h.E;
   a.G = h.G;
   a.slots = h.slots;
-  a.chunk = place_chunk(h.E, h.G);
+  a.chunk = place_chunk_experts(h.S, h.E, h.G);
   for (int g = 0; g < h.G; ++g) a.cap[g] = h.cap[g];
   const size_t lds = place_lds_bytes(h.S, h.E, h.G);
   static bool attr_set = false;
