@@ -64,7 +64,9 @@ def lib():
                                                              _i32p, _f64p]
         L.oracle_place_greedy.argtypes = [C.c_int] * 4 + [_i64p, _vp, _f64p, _vp, C.c_double, _i32p, _i32p,
                                                           C.c_double, C.c_double, C.c_double, _i32p, _vp]
-        for name in ("oracle_place_objective", "oracle_place_greedy", "oracle_route", "oracle_route_stats", "oracle_permute", "oracle_gather_rows",
+        L.oracle_window_stats.argtypes = [C.c_int] * 4 + [_i64p, _vp, _i32p, _i32p, _vp, C.c_int, _i64p, _i64p,
+                                                          _i64p, _vp]
+        for name in ("oracle_window_stats", "oracle_place_objective", "oracle_place_greedy", "oracle_route", "oracle_route_stats", "oracle_permute", "oracle_gather_rows",
                      "oracle_swiglu_hidden", "oracle_linear", "oracle_swiglu_ffn", "oracle_ffn_rows",
                      "oracle_combine", "oracle_forward_tokens"):
             getattr(L, name).restype = C.c_int
@@ -243,3 +245,23 @@ def place_greedy(A, D, x0, cap, B=None, M=None, m_uniform: float = 1.0,
                                      float(alpha), float(beta), float(gamma), x, _ptr(score)),
            "oracle_place_greedy")
     return x[:L], score[:L]
+
+
+def window_stats(A, x, home, G, B=None, engine=None, n_eng=None, pressure=True):
+    """(remote [L,S], total [L,S], rank_load [L,G], pressure [n_eng] or None)."""
+    A = _c(A, np.int64)
+    if A.ndim == 2:
+        A = A[None]
+    L, S, E = A.shape
+    x = _c(x, np.int32).reshape(L, E)
+    home = _c(home, np.int32)
+    B = None if B is None else _c(B, np.int64).reshape(L, E)
+    eng = None if engine is None else _c(engine, np.int32)
+    n_eng = G if n_eng is None else n_eng
+    remote = np.empty((max(L, 1), S), np.int64)
+    total = np.empty((max(L, 1), S), np.int64)
+    rank_load = np.empty((max(L, 1), G), np.int64)
+    pr = np.empty(n_eng, np.float64) if pressure else None
+    _check(lib().oracle_window_stats(L, S, E, G, A, _ptr(B), x, home, _ptr(eng), n_eng, remote, total,
+                                     rank_load, _ptr(pr)), "oracle_window_stats")
+    return remote[:L], total[:L], rank_load[:L], pr

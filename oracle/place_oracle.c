@@ -276,3 +276,84 @@ done:
     free(load);
     return rc;
 }
+
+/*
+ * Window diagnostics under a placement.
+ *   remote [L][S] int64: tokens of source s routed to experts that are not on
+ *                        the source's own rank home[s] (the share of traffic
+ *                        crossing to other DP groups, Sec. 2.2, Fig. 4);
+ *   total  [L][S] int64: all tokens of source s (sum_e A);
+ *   rank_load [L][G] int64: B summed over the experts placed on each rank
+ *                        (the tokens the rank's experts process);
+ *   pressure [n_eng] double, nullable: the MoE pressure of each DP engine
+ *                        (Sec. 4.1), read as its ranks' token load over the
+ *                        window, all layers, relative to the average engine:
+ *                        load_d / ((sum_d' load_d') / n_eng); 0 when no load.
+ * x[l][e] outside [0, G) hosts the expert nowhere: its tokens are remote for
+ * every source and load no rank.  home[s] outside [0, G) makes all of source
+ * s's tokens remote.  engine (nullable, [G]) maps each rank to its DP engine
+ * (NULL: rank g is engine g, n_eng = G); a rank mapped outside [0, n_eng)
+ * belongs to no engine.
+ *
+ * Pinned by: a hand-worked instance from the paper's example statistics; the
+ * remote tokens equal the objective's C_comm for the 0/1 cost "not the
+ * source's rank"; rank loads add up to the total load; pressures average to
+ * one; placing every expert on one source's rank leaves that source nothing
+ * remote.
+ */
+int oracle_window_stats(int L, int S, int E, int G, const int64_t *A,
+                        const int64_t *B, const int32_t *x,
+                        const int32_t *home, const int32_t *engine, int n_eng,
+                        int64_t *remote, int64_t *total, int64_t *rank_load,
+                        double *pressure)
+{
+    if (!place_dims_ok(L, S, E, G) || n_eng < 1 || (!engine && n_eng != G))
+        return ORACLE_ERR_DIMS;
+    for (int l = 0; l < L; ++l) {
+        const int64_t *Al = A + (size_t)l * S * E;
+        const int32_t *xl = x + (size_t)l * E;
+        for (int s = 0; s < S; ++s) {
+            int64_t rem = 0, tot = 0;
+            for (int e = 0; e < E; ++e) {
+                int64_t a = Al[(size_t)s * E + e];
+                tot += a;
+                if (xl[e] != home[s] || home[s] < 0 || home[s] >= G)
+                    rem += a;
+            }
+            remote[(size_t)l * S + s] = rem;
+            total[(size_t)l * S + s] = tot;
+        }
+        for (int g = 0; g < G; ++g) {
+            int64_t load = 0;
+            for (int e = 0; e < E; ++e) {
+                if (xl[e] != g)
+                    continue;
+                int64_t b = 0;
+                if (B) {
+                    b = B[(size_t)l * E + e];
+                } else {
+                    for (int s = 0; s < S; ++s)
+                        b += Al[(size_t)s * E + e];
+                }
+                load += b;
+            }
+            rank_load[(size_t)l * G + g] = load;
+        }
+    }
+    if (pressure) {
+        int64_t all = 0;
+        for (int d = 0; d < n_eng; ++d) {
+            int64_t load = 0;
+            for (int l = 0; l < L; ++l)
+                for (int g = 0; g < G; ++g)
+                    if ((engine ? engine[g] : g) == d)
+                        load += rank_load[(size_t)l * G + g];
+            pressure[d] = (double)load;
+            all += load;
+        }
+        double mean = (double)all / n_eng;
+        for (int d = 0; d < n_eng; ++d)
+            pressure[d] = all == 0 ? 0.0 : pressure[d] / mean;
+    }
+    return ORACLE_OK;
+}

@@ -62,6 +62,13 @@ PLACE_MUTANTS = [(PLACE_SRC,) + m for m in [
     ("beta_dropped", "score = score + beta * c_load;", "score = score + c_load;", 0),
     ("objective_mean_wrong", "mean /= G;", "mean /= (G + 1);", 0),
     ("objective_mig_signed", "* fabs(xi - x0i);", "* (xi - x0i);", 0),
+    ("window_home_inverted", "if (xl[e] != home[s] || home[s] < 0", "if (xl[e] == home[s] || home[s] < 0", 0),
+    ("window_total_only_remote", "tot += a;", "tot += a * (xl[e] != home[s]);", 0),
+    ("window_load_one_source", "                        b += Al[(size_t)s * E + e];",
+     "                        b += Al[e];", 0),
+    ("window_b_ignored", "b = B[(size_t)l * E + e];", "b = Al[e];", 0),
+    ("window_pressure_raw", "pressure[d] / mean;", "pressure[d];", 0),
+    ("window_engine_ignored", "if ((engine ? engine[g] : g) == d)", "if (g == d)", 0),
     ("objective_comm_ignores_x", "D[(size_t)s * G + g] *\n                              (xl[e] == g ? 1.0 : 0.0);",
      "D[(size_t)s * G + g] *\n                              (xl[e] == g ? 1.0 : 1.0);", 0),
 ]]

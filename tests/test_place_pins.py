@@ -282,3 +282,83 @@ def test_infeasible_capacity_is_rejected(oracle_mod):
     with pytest.raises(oracle_mod.OracleError):
         oracle_mod.place_greedy(np.zeros((1, 1, 5), np.int64), np.zeros((1, 2)), np.zeros((1, 5), np.int32),
                                 np.array([2, 2], np.int32))
+
+
+# ------------------------------------------------- window diagnostics -------
+
+def test_window_worked_example(oracle_mod):
+    g = _golden()
+    w = g["window"]
+    remote, total, rank_load, pressure = oracle_mod.window_stats(
+        np.array(g["A"]), np.array(w["x"]), np.array(w["home"]), 2, B=np.array(g["B"]))
+    assert remote[0].tolist() == w["remote"], w["derivation"]
+    assert total[0].tolist() == w["total"]
+    assert rank_load[0].tolist() == w["rank_load"]
+    assert pressure.tolist() == pytest.approx([a / b for a, b in w["pressure_fraction"]], rel=1e-15)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_window_remote_is_objective_comm(oracle_mod, seed):
+    """With D_{s,g} = [g is not source s's rank], the remote tokens of all
+    sources add up to the objective's C_comm (an independent function)."""
+    rng = np.random.default_rng(500 + seed)
+    L, S, E, G = 3, 6, 20, 4
+    A = rng.integers(0, 1000, size=(L, S, E)).astype(np.int64)
+    x = rng.integers(0, G, size=(L, E)).astype(np.int32)
+    home = rng.integers(0, G, size=S).astype(np.int32)
+    D = np.ones((S, G))
+    D[np.arange(S), home] = 0.0
+    remote, total, _, _ = oracle_mod.window_stats(A, x, home, G)
+    terms = oracle_mod.place_objective(A, D, x, x)
+    assert remote.sum(axis=1).tolist() == terms[:, 0].tolist()
+    assert (total == A.sum(axis=2)).all()
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_window_loads_and_pressure(oracle_mod, seed):
+    rng = np.random.default_rng(600 + seed)
+    L, S, E, G = 4, 3, 24, 6
+    A = rng.integers(0, 500, size=(L, S, E)).astype(np.int64)
+    B = rng.integers(0, 9000, size=(L, E)).astype(np.int64) if seed % 2 else None
+    x = rng.integers(0, G, size=(L, E)).astype(np.int32)
+    _, _, rank_load, pressure = oracle_mod.window_stats(A, x, np.zeros(S, np.int32), G, B=B)
+    load = A.sum(axis=1) if B is None else B
+    assert (rank_load.sum(axis=1) == load.sum(axis=1)).all()
+    for l in range(L):
+        assert rank_load[l].tolist() == np.bincount(x[l], weights=load[l], minlength=G).astype(np.int64).tolist()
+    assert pressure.mean() == pytest.approx(1.0, rel=1e-12)
+    assert pressure.tolist() == pytest.approx((rank_load.sum(0) / rank_load.sum(0).mean()).tolist(), rel=1e-15)
+    # two engines of three ranks each (TP groups): pressure of the sums
+    engine = np.array([0, 0, 0, 1, 1, 1], np.int32)
+    _, _, _, p2 = oracle_mod.window_stats(A, x, np.zeros(S, np.int32), G, B=B, engine=engine, n_eng=2)
+    per = rank_load.sum(0)
+    eng = np.array([per[:3].sum(), per[3:].sum()], np.float64)
+    assert p2.tolist() == pytest.approx((eng / eng.mean()).tolist(), rel=1e-15)
+
+
+def test_window_all_experts_home(oracle_mod):
+    """Every expert on source 2's rank: nothing of source 2 is remote, all of
+    every other source is; only that rank carries load."""
+    rng = np.random.default_rng(7)
+    L, S, E, G = 2, 4, 10, 4
+    A = rng.integers(1, 100, size=(L, S, E)).astype(np.int64)
+    home = np.arange(S, dtype=np.int32)
+    remote, total, rank_load, pressure = oracle_mod.window_stats(A, np.full((L, E), 2, np.int32), home, G)
+    assert (remote[:, 2] == 0).all()
+    assert (remote[:, [0, 1, 3]] == total[:, [0, 1, 3]]).all()
+    assert (rank_load[:, [0, 1, 3]] == 0).all()
+    assert pressure.tolist() == [0.0, 0.0, 4.0, 0.0]
+
+
+def test_window_unplaced_and_homeless(oracle_mod):
+    """An expert hosted nowhere is remote for every source and loads no rank;
+    a source without a rank has all of its traffic remote; no load at all
+    gives zero pressure."""
+    A = np.array([[[5, 7, 11]]], np.int64)
+    remote, total, rank_load, pressure = oracle_mod.window_stats(A, np.array([[0, -1, 9]]), np.array([0]), 2)
+    assert remote.tolist() == [[18]] and total.tolist() == [[23]] and rank_load.tolist() == [[5, 0]]
+    remote, _, _, _ = oracle_mod.window_stats(A, np.array([[0, 0, 1]]), np.array([-3]), 2)
+    assert remote.tolist() == [[23]]
+    _, _, _, pressure = oracle_mod.window_stats(np.zeros((1, 1, 3), np.int64), np.array([[0, 1, 1]]),
+                                                np.array([0]), 2)
+    assert pressure.tolist() == [0.0, 0.0]
