@@ -109,10 +109,16 @@ def stage_work(cfg, R: int, active: int) -> dict:
     return w
 
 
-def source_digest() -> str:
+# The sources of the layer's kernels: a profile's counters stay valid while
+# these are unchanged (placement and diagnostics kernels do not run in a step).
+LAYER_SOURCES = ("common.h", "ffn_impl.h", "route.hip", "permute.hip", "ffn_skinny.hip", "ffn_tiled.hip",
+                 "combine.hip")
+
+
+def source_digest(names=LAYER_SOURCES) -> str:
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2606_15177_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
+    for name in sorted(names):
         with open(os.path.join(csrc, name), "rb") as f:
             h.update(name.encode() + f.read())
     return h.hexdigest()[:16]
@@ -192,6 +198,25 @@ def bench_place(args) -> int:
     events.close()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     moved = float((x.cpu().numpy() != p["x0"]).mean())
+
+    # what the window's statistics say before and after: the share of traffic
+    # that leaves its source's rank, and the spread of the engines' MoE pressure
+    home = torch.from_numpy((np.arange(cfg.S) * cfg.G // cfg.S).astype(np.int32)).cuda()
+    wd = moe.MoeWindowDims(cfg.L, cfg.S, cfg.E, cfg.G, cfg.G)
+
+    def window(placement):
+        remote = torch.empty((cfg.L, cfg.S), dtype=torch.int64, device="cuda")
+        total = torch.empty_like(remote)
+        rank_load = torch.empty((cfg.L, cfg.G), dtype=torch.int64, device="cuda")
+        pressure = torch.empty((cfg.G,), dtype=torch.float64, device="cuda")
+        moe.window_stats(wd, A, placement, home, remote, total, rank_load, pressure=pressure)
+        torch.cuda.synchronize()
+        return {"remote_fraction": round(float(remote.sum()) / max(float(total.sum()), 1.0), 4),
+                "max_rank_load_over_mean": round(float((rank_load.double().max(dim=1).values /
+                                                        rank_load.double().mean(dim=1)).mean()), 4),
+                "pressure_max": round(float(pressure.max()), 4), "pressure_min": round(float(pressure.min()), 4)}
+
+    diagnostics = {"before": window(x0), "after": window(x)}
     result = {
         "metric": "expert placement: MoE layers placed per second on 1 MI355X",
         "value": round(cfg.L / (ms_per_step * 1e-3), 1),
@@ -213,6 +238,7 @@ def bench_place(args) -> int:
         "roofline": {"bound": "latency", "kernel": "place", "kernel_ms": round(kernel_ms, 4),
                      "ns_per_expert_step": round(kernel_ms * 1e6 / cfg.E, 1)},
         "moved_fraction": round(moved, 4),
+        "window": diagnostics,
         "device": torch.cuda.get_device_name(0),
     }
     if not args.no_cpu_baseline:

@@ -322,6 +322,54 @@ int moe_place_experts(const moe_place_dims *dims, const int32_t *cap,
                       const double *M, const int32_t *x0, int32_t *x,
                       int32_t *rank_experts, double *cost, void *stream);
 
+/*
+ * ---- Window diagnostics under a placement (Sec. 2.2 Fig. 4; Sec. 4.1; Sec. 6)
+ *
+ * What a profiling window's statistics say about a placement x (for instance
+ * the current one, or the one moe_place_experts proposes):
+ *   - the traffic of each source that crosses to experts outside the source's
+ *     own rank (the share of a DP group's MoE traffic sent to remote DP groups
+ *     that motivates source-aware placement, Sec. 2.2, Fig. 4);
+ *   - the token load each rank's experts process;
+ *   - the MoE pressure each DP engine reports to the scheduler (Sec. 4.1): the
+ *     token-equivalent expert load of the engine's ranks, all layers of the
+ *     window, divided by the average over engines (1.0 = average; Sec. 6
+ *     feeds it back as a relative penalty).
+ */
+typedef struct moe_window_dims {
+    int32_t L;          /* layers, >= 0 */
+    int32_t S;          /* source DP engines, >= 1 */
+    int32_t E;          /* experts per layer, 1..8192 */
+    int32_t G;          /* EP ranks, 1..1024 */
+    int32_t n_engines;  /* DP engines the ranks belong to, 1..1024 */
+} moe_window_dims;
+
+/*
+ *   A          [L][S][E] int64: the window's source x expert counts.
+ *   B          [L][E] int64, nullable: aggregate loads (NULL = column sums of A).
+ *   x          [L][E] int32: the rank hosting each expert; a value outside
+ *              [0, G) hosts it nowhere (its tokens are remote for every
+ *              source and load no rank).
+ *   home       [S] int32: the EP rank co-located with each source's DP engine;
+ *              outside [0, G) makes all of that source's traffic remote.
+ *   engine     [G] int32, nullable: the DP engine (TP group) each rank belongs
+ *              to, ranks mapped outside [0, n_engines) belong to none; NULL
+ *              means rank g is engine g and requires n_engines == G.
+ *   remote     [L][S] int64 out: sum_e A[l][s][e] over experts not on home[s].
+ *   total      [L][S] int64 out: sum_e A[l][s][e].
+ *   rank_load  [L][G] int64 out: sum of B[l][e] over the experts on rank g.
+ *   pressure   [n_engines] fp64 out, nullable: engine load (its ranks'
+ *              rank_load over all layers) / (all engines' load / n_engines),
+ *              one IEEE division each; 0 when there is no load at all.
+ * Integer results are exact (sums of int64, any order).  int64 and fp64
+ * arrays 8-byte aligned, int32 arrays 4-byte aligned (MOE_ERR_ALIGN).  With
+ * L = 0 only the pressure (all zeros) is written.
+ */
+int moe_window_stats(const moe_window_dims *dims, const int64_t *A,
+                     const int64_t *B, const int32_t *x, const int32_t *home,
+                     const int32_t *engine, int64_t *remote, int64_t *total,
+                     int64_t *rank_load, double *pressure, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -21,7 +21,7 @@ LIB_NAME = "libmoe_gfx950.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
 ARCH = "gfx950"
 
-SOURCES = ["route.hip", "permute.hip", "combine.hip", "ffn_skinny.hip", "ffn_tiled.hip", "place.hip",
+SOURCES = ["route.hip", "permute.hip", "combine.hip", "ffn_skinny.hip", "ffn_tiled.hip", "place.hip", "window.hip",
            "moe_abi.hip"]
 
 CXXFLAGS = [

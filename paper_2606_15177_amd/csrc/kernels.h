@@ -117,4 +117,23 @@ struct PlaceArgs {
 size_t place_lds_bytes(int S, int E, int G);
 hipError_t launch_place(const PlaceArgs& a, hipStream_t st);
 
+// ---- window.hip ------------------------------------------------------------
+// Window diagnostics under a placement (see moe.h).
+constexpr int kWindowMaxExperts = 8192;
+constexpr int kWindowMaxRanks = 1024;
+constexpr int kWindowMaxEngines = 1024;
+struct WindowArgs {
+  int L, S, E, G, n_engines;
+  const int64_t* A;       // [L][S][E]
+  const int64_t* B;       // [L][E] or null
+  const int32_t* x;       // [L][E]
+  const int32_t* home;    // [S]
+  const int32_t* engine;  // [G] or null (rank g is engine g)
+  int64_t* remote;        // [L][S]
+  int64_t* total;         // [L][S]
+  int64_t* rank_load;     // [L][G]
+  double* pressure;       // [n_engines] or null
+};
+hipError_t launch_window(const WindowArgs& a, hipStream_t st);
+
 }  // namespace moe

@@ -399,4 +399,24 @@ int moe_place_experts(const moe_place_dims* pd, const int32_t* cap, const int64_
   return status(moe::launch_place(a, static_cast<hipStream_t>(stream)));
 }
 
+int moe_window_stats(const moe_window_dims* wd, const int64_t* A, const int64_t* B, const int32_t* x,
+                     const int32_t* home, const int32_t* engine, int64_t* remote, int64_t* total,
+                     int64_t* rank_load, double* pressure, void* stream) {
+  if (wd == nullptr) return MOE_ERR_NULL;
+  if (wd->L < 0 || wd->S < 1 || wd->E < 1 || wd->G < 1 || wd->n_engines < 1) return MOE_ERR_DIMS;
+  if (engine == nullptr && wd->n_engines != wd->G) return MOE_ERR_DIMS;
+  if (wd->E > moe::kWindowMaxExperts || wd->G > moe::kWindowMaxRanks ||
+      wd->n_engines > moe::kWindowMaxEngines ||
+      static_cast<int64_t>(wd->L) * wd->S * wd->E > (int64_t{1} << 40))
+    return MOE_ERR_UNSUPPORTED;
+  if (wd->L > 0 && (!A || !x || !home || !remote || !total || !rank_load)) return MOE_ERR_NULL;
+  auto al = [](const void* p, uintptr_t n) { return (reinterpret_cast<uintptr_t>(p) & (n - 1)) == 0; };
+  if (!al(A, 8) || !al(B, 8) || !al(remote, 8) || !al(total, 8) || !al(rank_load, 8) || !al(pressure, 8) ||
+      !al(x, 4) || !al(home, 4) || !al(engine, 4))
+    return MOE_ERR_ALIGN;
+  moe::WindowArgs a{wd->L, wd->S, wd->E, wd->G, wd->n_engines, A, B, x, home, engine,
+                    remote, total, rank_load, pressure};
+  return status(moe::launch_window(a, static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

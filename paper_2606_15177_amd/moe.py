@@ -44,6 +44,10 @@ class MoePlaceDims(C.Structure):
                 ("m_uniform", C.c_double)]
 
 
+class MoeWindowDims(C.Structure):
+    _fields_ = [(n, C.c_int32) for n in ("L", "S", "E", "G", "n_engines")]
+
+
 class MoeError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
@@ -70,6 +74,7 @@ def _load() -> C.CDLL:
                          vp, sz, vp], i32),
         "moe_place_slots": ([C.POINTER(MoePlaceDims), vp], sz),
         "moe_place_experts": ([C.POINTER(MoePlaceDims), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp], i32),
+        "moe_window_stats": ([C.POINTER(MoeWindowDims), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp], i32),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -229,6 +234,17 @@ def place_experts(pd: MoePlaceDims, cap, A, D, x0, x, B=None, M=None, rank_exper
     _check(_lib.moe_place_experts(C.byref(pd), cap_p, _ptr(A, _I64), _ptr(B, _I64), _ptr(D, _F64),
                                   _ptr(M, _F64), _ptr(x0, _I32), _ptr(x, _I32), _ptr(rank_experts, _I32),
                                   _ptr(cost, _F64), _stream(stream)), "moe_place_experts")
+
+
+def window_stats(wd: MoeWindowDims, A, x, home, remote, total, rank_load, B=None, engine=None, pressure=None,
+                 stream=None):
+    """moe_window_stats: every tensor on the GPU (A int64 [L,S,E], x int32
+    [L,E], home int32 [S], engine int32 [G]; outputs remote/total int64 [L,S],
+    rank_load int64 [L,G], pressure fp64 [n_engines])."""
+    _check(_lib.moe_window_stats(C.byref(wd), _ptr(A, _I64), _ptr(B, _I64), _ptr(x, _I32), _ptr(home, _I32),
+                                 _ptr(engine, _I32), _ptr(remote, _I64), _ptr(total, _I64),
+                                 _ptr(rank_load, _I64), _ptr(pressure, _F64), _stream(stream)),
+           "moe_window_stats")
 
 
 class MoeLayer:

@@ -155,3 +155,31 @@ def test_place_checks_alignment_and_noop(moe):
     pd0 = moe.place_dims(L=0, S=2, E=8, G=2)
     assert lib.moe_place_experts(C.byref(pd0), cap_p, None, None, None, None, None, None, None, None,
                                  None) == moe.MOE_OK
+
+
+@pytest.mark.parametrize("change,engine,code", [
+    (dict(L=-1), False, -2), (dict(S=0), False, -2), (dict(E=0), False, -2), (dict(G=0, n_engines=0), False, -2),
+    (dict(n_engines=0), True, -2),
+    (dict(n_engines=3), False, -2),          # no engine map: engines must be the ranks
+    (dict(E=8193), False, -3), (dict(G=1025, n_engines=1025), False, -3), (dict(n_engines=1025), True, -3),
+    (dict(), False, -1),                     # outputs missing
+])
+def test_window_rejects_before_launch(moe, change, engine, code):
+    base = dict(L=2, S=2, E=8, G=4, n_engines=4)
+    base.update(change)
+    wd = moe.MoeWindowDims(**base)
+    rc = moe._lib.moe_window_stats(C.byref(wd), None, None, None, None, 16 if engine else None, None, None, None,
+                                   None, None)
+    assert rc == code
+
+
+def test_window_alignment_and_empty(moe):
+    lib = moe._lib
+    wd = moe.MoeWindowDims(L=2, S=2, E=8, G=4, n_engines=4)
+    assert lib.moe_window_stats(None, 16, None, 16, 16, None, 16, 16, 16, None, None) == moe.MOE_ERR_NULL
+    assert lib.moe_window_stats(C.byref(wd), 20, None, 16, 16, None, 16, 16, 16, None, None) == moe.MOE_ERR_ALIGN
+    assert lib.moe_window_stats(C.byref(wd), 16, None, 18, 16, None, 16, 16, 16, None, None) == moe.MOE_ERR_ALIGN
+    assert lib.moe_window_stats(C.byref(wd), 16, None, 16, 16, None, 16, 16, 16, 12, None) == moe.MOE_ERR_ALIGN
+    wd0 = moe.MoeWindowDims(L=0, S=2, E=8, G=4, n_engines=4)
+    assert lib.moe_window_stats(C.byref(wd0), None, None, None, None, None, None, None, None, None,
+                                None) == moe.MOE_OK
