@@ -138,6 +138,54 @@ def measured_traffic(stage: str, workload: str):
     return float(m_b.group(1))
 
 
+def sample_gpu_metrics(busy_step, max_s: float = 20.0) -> dict:
+    """Clock and power of GPU 0 sampled by amd-smi while busy_step() keeps the
+    GPU busy (best effort: an empty dict when the tool is missing or fails)."""
+    import subprocess
+    import threading
+
+    import torch
+    out = {}
+
+    def sample():
+        try:
+            r = subprocess.run(["amd-smi", "metric", "-c", "-p", "--json", "-g", "0"], capture_output=True,
+                               text=True, timeout=max_s)
+            out["raw"] = r.stdout
+        except Exception as e:  # noqa: BLE001 - a missing tool only loses the sample
+            out["error"] = str(e)
+
+    th = threading.Thread(target=sample)
+    th.start()
+    t0 = time.perf_counter()
+    while th.is_alive() and time.perf_counter() - t0 < max_s + 5:
+        for _ in range(20):
+            busy_step()
+        torch.cuda.synchronize()
+    th.join(timeout=1.0)
+    res = {}
+    try:
+        data = json.loads(out.get("raw", ""))
+        gpu = data[0] if isinstance(data, list) else data
+        if isinstance(gpu, dict) and "gpu_data" in gpu:
+            gpu = gpu["gpu_data"][0]
+
+        def val(d, *keys):
+            for k in keys:
+                if not isinstance(d, dict) or k not in d:
+                    return None
+                d = d[k]
+            return d.get("value") if isinstance(d, dict) else d
+
+        res = {"sclk_mhz": val(gpu, "clock", "gfx_0", "clk"), "mclk_mhz": val(gpu, "clock", "mem_0", "clk"),
+               "socket_power_w": val(gpu, "power", "socket_power")}
+    except Exception:  # noqa: BLE001
+        res = {}
+    if not any(v is not None for v in res.values()):
+        res = {"unparsed": (out.get("raw") or out.get("error") or "")[:400]}
+    return res
+
+
 def cpu_baseline(cfg, wl, budget_s: float) -> dict:
     """The CPU oracle (plain C, fp64, single thread) on a bounded sample of
     the same workload: the first n tokens, n sized to the time budget."""
@@ -314,6 +362,28 @@ def main(argv=None) -> int:
     for s_i, name in enumerate(STAGES):
         vals = [probe_ev.elapsed_ms(i * n_ev + 2 * s_i, i * n_ev + 2 * s_i + 1) for i in range(n_probe)]
         stage_ms[name] = sum(vals) / len(vals)
+    # GPU time of each probe step: first stage's start to the last stage's end
+    probe_steps = sorted(probe_ev.elapsed_ms(i * n_ev, i * n_ev + n_ev - 1) for i in range(n_probe))
+    # the same probe without the source x expert statistics (the counting that
+    # the route kernel fuses): its route time against the one above is the
+    # cost of collecting A
+    for i in range(n_probe):
+        layer.forward(logits, src, x, None, out,
+                      moe.make_taps(offsets=offsets, events=probe_ev.ev[i * n_ev:(i + 1) * n_ev]))
+    torch.cuda.synchronize()
+    route_no_stats = sum(probe_ev.elapsed_ms(i * n_ev, i * n_ev + 1) for i in range(n_probe)) / n_probe
+    # cold steps: a 1 GiB write before each step evicts the L2s and the
+    # Infinity Cache, so every input comes from HBM
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    cold = []
+    for i in range(n_probe):
+        flush.fill_(i & 0xFF)
+        layer.forward(logits, src, x, counts, out,
+                      moe.make_taps(offsets=offsets, events=probe_ev.ev[i * n_ev:(i + 1) * n_ev]))
+        torch.cuda.synchronize()
+        cold.append(probe_ev.elapsed_ms(i * n_ev, i * n_ev + n_ev - 1))
+    del flush
+    cold.sort()
     probe_ev.close()
     dom = max(STAGES, key=lambda n: stage_ms[n])
     dom_i = STAGES.index(dom)
@@ -367,6 +437,8 @@ def main(argv=None) -> int:
     ffn_bytes = work["ffn_up"]["bytes"] + work["ffn_down"]["bytes"]
     ffn_frac_hbm = ffn_bytes / (ffn_ms * 1e-3) / (HBM_PEAK_GBS * 1e9) if ffn_ms > 0 else 0.0
 
+    metrics = sample_gpu_metrics(lambda: layer.forward(logits, src, x, counts, out, plain_taps))
+
     if args.calib_copy_mib:
         n = args.calib_copy_mib * (1 << 20)
         a = torch.empty(n, dtype=torch.uint8, device="cuda")
@@ -398,6 +470,14 @@ def main(argv=None) -> int:
                                    "permute": stages["permute"]["frac_hbm"],
                                    "combine": stages["combine"]["frac_hbm"]},
         "stages": stages,
+        "step_gpu_ms": {"median": round(probe_steps[len(probe_steps) // 2], 4), "min": round(probe_steps[0], 4),
+                        "samples": len(probe_steps)},
+        "cold": {"median_ms": round(cold[len(cold) // 2], 4), "min_ms": round(cold[0], 4),
+                 "tokens_per_s": round(cfg.T / (cold[len(cold) // 2] * 1e-3), 1),
+                 "note": "1 GiB written before each step; GPU time of the step"},
+        "stats_collection": {"route_ms_with_counts": round(stage_ms["route"], 4),
+                             "route_ms_without_counts": round(route_no_stats, 4)},
+        "gpu_metrics": metrics,
         "rows_local": R,
         "active_experts": active,
         "device": torch.cuda.get_device_name(0),
