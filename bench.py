@@ -46,25 +46,33 @@ def parse_args(argv=None):
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="budget of the CPU-oracle baseline sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--fenced-events", action="store_true",
+                   help="time with default (system-fenced) HIP events instead of timing-only ones")
     p.add_argument("--calib-copy-mib", type=int, default=0,
                    help="also run a plain device copy of this size (HBM counter calibration)")
     return p.parse_args(argv)
 
 
+# Timing-only events: no system-scope fence (cache writeback and invalidate)
+# when the event is recorded, so recording one does not stall the stream; the
+# host reads the times only after a device-wide synchronisation.
+HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000
+
+
 class HipEvents:
     """hipEvent_t handles from the HIP runtime the process already uses."""
 
-    def __init__(self, n: int):
+    def __init__(self, n: int, flags: int = HIP_EVENT_DISABLE_SYSTEM_FENCE):
         import torch  # noqa: F401  (loads torch's HIP runtime first)
         self.hip = ctypes.CDLL("libamdhip64.so.7")
-        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
         self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
                                                  ctypes.c_void_p]
         self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
         self.ev = []
         for _ in range(n):
             e = ctypes.c_void_p()
-            rc = self.hip.hipEventCreate(ctypes.byref(e))
+            rc = self.hip.hipEventCreateWithFlags(ctypes.byref(e), flags)
             if rc != 0:
                 raise RuntimeError(f"hipEventCreate failed ({rc})")
             self.ev.append(e.value)
@@ -353,7 +361,8 @@ def main(argv=None) -> int:
     # stage (ten event records cost several percent of a decode step, so the
     # timed steps carry only the dominant kernel's pair).
     n_probe = max(3, min(args.steps, 10))
-    probe_ev = HipEvents(n_ev * n_probe)
+    ev_flags = 0 if args.fenced_events else HIP_EVENT_DISABLE_SYSTEM_FENCE
+    probe_ev = HipEvents(n_ev * n_probe, ev_flags)
     for i in range(n_probe):
         layer.forward(logits, src, x, counts, out,
                       moe.make_taps(offsets=offsets, events=probe_ev.ev[i * n_ev:(i + 1) * n_ev]))
@@ -388,7 +397,7 @@ def main(argv=None) -> int:
     dom = max(STAGES, key=lambda n: stage_ms[n])
     dom_i = STAGES.index(dom)
 
-    events = HipEvents(2 * args.steps)
+    events = HipEvents(2 * args.steps, ev_flags)
     step_taps = []
     for i in range(args.steps):
         ev = [None] * n_ev
