@@ -112,6 +112,150 @@ int oracle_route(int T, int E, int k, const float *logits,
 }
 
 /*
+ * Gating variants (Sec. 2.1 names a router that picks each token's top-k
+ * experts but not its gating function; three common ones are written out
+ * here).  gate selects:
+ *   0  softmax over the k selected logits (renormalised; oracle_route);
+ *   1  softmax over all E logits, evaluated at the k selected experts (not
+ *      renormalised): w_j = exp(l_j - M) / sum_e exp(l_e - M), M the largest
+ *      logit that is a number;
+ *   2  sigmoid scores s_e = sigma(l_e), evaluated in fp64 and rounded to fp32;
+ *      experts are selected by s_e + bias_e (fp32 sum; bias nullable, used
+ *      for the selection only) and weighted w_j = s_j / sum_j' s_j'.
+ * Selection is by the selection value c_e (l_e for gates 0 and 1, s_e + bias_e
+ * for gate 2) under the total order of comes_before (value descending, lower
+ * index first, NaN last).  With n_group > 1 the experts form n_group groups
+ * of E / n_group consecutive ids; a group's score is the fp32 sum of its two
+ * first selection values in that order (its one value when groups hold a
+ * single expert); the first topk_group groups in the order of comes_before
+ * over group scores stay, and the k experts are selected among theirs.  All
+ * gates are finally multiplied by scale.
+ *
+ * Pinned by: brute-force enumeration of the kept group set and of the
+ * selected experts; the full softmax of a library routine evaluated at the
+ * selected experts; sigmoid gates in closed form; the bias moving the
+ * selection but not the gates; n_group = 1 and topk_group = n_group reducing
+ * to the ungrouped selection; a hand-worked grouped example.
+ */
+int oracle_route_gated(int T, int E, int k, int gate, const float *logits,
+                       const float *bias, double scale, int n_group,
+                       int topk_group, int32_t *topk_idx, double *topk_w)
+{
+    if (T < 0 || E < 1 || k < 1 || k > E || gate < 0 || gate > 2)
+        return ORACLE_ERR_DIMS;
+    if (bias && gate != 2)
+        return ORACLE_ERR_DIMS;
+    int grouped = n_group > 1;
+    int gsz = grouped ? E / n_group : E;
+    if (grouped && (E % n_group != 0 || topk_group < 1 || topk_group > n_group ||
+                    k > topk_group * gsz))
+        return ORACLE_ERR_DIMS;
+    int rc = ORACLE_OK;
+    float *c = (float *)malloc(sizeof(float) * (size_t)E);
+    double *sg = (double *)malloc(sizeof(double) * (size_t)E);
+    char *allowed = (char *)malloc((size_t)E);
+    char *taken = (char *)malloc((size_t)E);
+    float *gscore = (float *)malloc(sizeof(float) * (size_t)(grouped ? n_group : 1));
+    char *gtaken = (char *)malloc((size_t)(grouped ? n_group : 1));
+    if (!c || !sg || !allowed || !taken || !gscore || !gtaken) {
+        rc = ORACLE_ERR_NOMEM;
+        goto done;
+    }
+    for (int t = 0; t < T; ++t) {
+        const float *row = logits + (size_t)t * E;
+        int32_t *idx = topk_idx + (size_t)t * k;
+        double *w = topk_w + (size_t)t * k;
+        /* selection values */
+        for (int e = 0; e < E; ++e) {
+            if (gate == 2) {
+                float s = (float)(1.0 / (1.0 + exp(-(double)row[e])));
+                sg[e] = (double)s;
+                c[e] = bias ? s + bias[e] : s;
+            } else {
+                c[e] = row[e];
+            }
+            allowed[e] = 1;
+        }
+        /* group limit: keep the topk_group best groups */
+        if (grouped) {
+            for (int q = 0; q < n_group; ++q) {
+                int first = -1, second = -1;
+                for (int e = q * gsz; e < (q + 1) * gsz; ++e) {
+                    if (first < 0 || comes_before(c[e], e, c[first], first)) {
+                        second = first;
+                        first = e;
+                    } else if (second < 0 || comes_before(c[e], e, c[second], second)) {
+                        second = e;
+                    }
+                }
+                gscore[q] = second < 0 ? c[first] : c[first] + c[second];
+                gtaken[q] = 0;
+            }
+            for (int j = 0; j < topk_group; ++j) {
+                int best = -1;
+                for (int q = 0; q < n_group; ++q) {
+                    if (gtaken[q])
+                        continue;
+                    if (best < 0 || comes_before(gscore[q], q, gscore[best], best))
+                        best = q;
+                }
+                gtaken[best] = 1;
+            }
+            for (int e = 0; e < E; ++e)
+                allowed[e] = gtaken[e / gsz];
+        }
+        /* the k first allowed experts */
+        memset(taken, 0, (size_t)E);
+        for (int j = 0; j < k; ++j) {
+            int best = -1;
+            for (int e = 0; e < E; ++e) {
+                if (taken[e] || !allowed[e])
+                    continue;
+                if (best < 0 || comes_before(c[e], e, c[best], best))
+                    best = e;
+            }
+            taken[best] = 1;
+            idx[j] = best;
+        }
+        /* gates */
+        if (gate == 0) {
+            double m = (double)row[idx[0]];
+            double sum = 0.0;
+            for (int j = 0; j < k; ++j)
+                sum += exp((double)row[idx[j]] - m);
+            for (int j = 0; j < k; ++j)
+                w[j] = exp((double)row[idx[j]] - m) / sum;
+        } else if (gate == 1) {
+            double m = NAN;
+            for (int e = 0; e < E; ++e)
+                if (!isnan(row[e]) && (isnan(m) || (double)row[e] > m))
+                    m = (double)row[e];
+            double sum = 0.0;
+            for (int e = 0; e < E; ++e)
+                sum += exp((double)row[e] - m);
+            for (int j = 0; j < k; ++j)
+                w[j] = exp((double)row[idx[j]] - m) / sum;
+        } else {
+            double sum = 0.0;
+            for (int j = 0; j < k; ++j)
+                sum += sg[idx[j]];
+            for (int j = 0; j < k; ++j)
+                w[j] = sg[idx[j]] / sum;
+        }
+        for (int j = 0; j < k; ++j)
+            w[j] *= scale;
+    }
+done:
+    free(c);
+    free(sg);
+    free(allowed);
+    free(taken);
+    free(gscore);
+    free(gtaken);
+    return rc;
+}
+
+/*
  * Source-aware routing statistics (Sec. 5.1).  counts is the S x E matrix A
  * of this layer and is accumulated (+=) so that successive calls form a
  * profiling window; counts[s][e] gains one for every selected pair (t, j)

@@ -50,6 +50,8 @@ def lib():
             build(force=False)
         L = C.CDLL(LIB)
         L.oracle_route.argtypes = [C.c_int, C.c_int, C.c_int, _f32p, _i32p, _f64p]
+        L.oracle_route_gated.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int, _f32p, _vp, C.c_double, C.c_int,
+                                         C.c_int, _i32p, _f64p]
         L.oracle_route_stats.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int, _i32p, _i32p, _i64p, _vp]
         L.oracle_permute.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int, _vp, _i32p, _i32p, _i32p, _i32p]
         L.oracle_gather_rows.argtypes = [C.c_int, C.c_int, _i32p, _u16p, _u16p]
@@ -66,7 +68,7 @@ def lib():
                                                           C.c_double, C.c_double, C.c_double, _i32p, _vp]
         L.oracle_window_stats.argtypes = [C.c_int] * 4 + [_i64p, _vp, _i32p, _i32p, _vp, C.c_int, _i64p, _i64p,
                                                           _i64p, _vp]
-        for name in ("oracle_window_stats", "oracle_place_objective", "oracle_place_greedy", "oracle_route", "oracle_route_stats", "oracle_permute", "oracle_gather_rows",
+        for name in ("oracle_route_gated", "oracle_window_stats", "oracle_place_objective", "oracle_place_greedy", "oracle_route", "oracle_route_stats", "oracle_permute", "oracle_gather_rows",
                      "oracle_swiglu_hidden", "oracle_linear", "oracle_swiglu_ffn", "oracle_ffn_rows",
                      "oracle_combine", "oracle_forward_tokens"):
             getattr(L, name).restype = C.c_int
@@ -99,6 +101,22 @@ def route(logits: np.ndarray, k: int):
     w = np.empty((T, k), np.float64)
     _check(lib().oracle_route(T, E, k, logits, idx, w), "oracle_route")
     return idx, w
+
+
+GATE_SOFTMAX_TOPK, GATE_SOFTMAX, GATE_SIGMOID = 0, 1, 2
+
+
+def route_gated(logits: np.ndarray, k: int, gate: int = GATE_SOFTMAX_TOPK, bias=None, scale: float = 1.0,
+                n_group: int = 0, topk_group: int = 0):
+    """Top-k ids [T, k] int32 and gates [T, k] fp64 under a gating variant."""
+    logits = _c(logits, np.float32)
+    T, E = logits.shape
+    b = None if bias is None else _c(bias, np.float32)
+    idx = np.empty((max(T, 1), k), np.int32)
+    w = np.empty((max(T, 1), k), np.float64)
+    _check(lib().oracle_route_gated(T, E, k, gate, logits, _ptr(b), float(scale), n_group, topk_group, idx, w),
+           "oracle_route_gated")
+    return idx[:T], w[:T]
 
 
 def route_stats(src: np.ndarray, topk_idx: np.ndarray, S: int, E: int, counts=None):

@@ -37,6 +37,16 @@ MUTANTS = [
      "if (s < 0)\n                s = idx[j] % E_local;\n            rc = oracle_swiglu_ffn", 0),
     ("shared_dropped", "for (int q = 0; q < n_sh; ++q) {", "for (int q = 0; q < 0; ++q) {", 0),
     ("combine_weight_dropped", "o[c] += w * bf16_value(", "o[c] += bf16_value(", 0),
+    ("group_score_max_only", "gscore[q] = second < 0 ? c[first] : c[first] + c[second];", "gscore[q] = c[first];", 0),
+    ("groups_worst_kept", "if (best < 0 || comes_before(gscore[q], q, gscore[best], best))",
+     "if (best < 0 || comes_before(gscore[best], best, gscore[q], q))", 0),
+    ("group_membership_strided", "allowed[e] = gtaken[e / gsz];", "allowed[e] = gtaken[e % n_group];", 0),
+    ("sigmoid_sign", "exp(-(double)row[e])", "exp((double)row[e])", 0),
+    ("bias_ignored", "c[e] = bias ? s + bias[e] : s;", "c[e] = s;", 0),
+    ("bias_in_gates", "w[j] = sg[idx[j]] / sum;", "w[j] = (double)c[idx[j]] / sum;", 0),
+    ("softmax_full_over_selected", "for (int e = 0; e < E; ++e)\n                sum += exp((double)row[e] - m);",
+     "for (int e = 0; e < k; ++e)\n                sum += exp((double)row[idx[e]] - m);", 0),
+    ("scale_dropped", "w[j] *= scale;", "w[j] *= 1.0;", 0),
 ]
 LAYER_MUTANTS = [(LAYER_SRC,) + m for m in MUTANTS]
 

@@ -394,3 +394,129 @@ def test_forward_tiny_config_matches_numpy_rederivation(oracle_mod):
         ref += ((order == e) * gates).sum(1)[:, None] * y
     err = np.abs(out - ref).max() / np.abs(ref).max()
     assert err < 1e-12, err
+
+
+# ------------------------------------------------------ gating variants ---
+
+def _gcase_arrays(case):
+    logits = _f32(case["logits"])[None, :]
+    bias = None if case["bias"] is None else _f32(case["bias"])
+    return logits, bias
+
+
+def test_route_gated_worked_examples(oracle_mod):
+    g = _load("route_worked.json")
+    for case in g["gated_cases"]:
+        logits, bias = _gcase_arrays(case)
+        idx, w = oracle_mod.route_gated(logits, case["k"], case["gate"], bias, case["scale"],
+                                        case["n_group"], case["topk_group"])
+        assert idx[0].tolist() == case["idx"], case["note"]
+        np.testing.assert_allclose(w[0], case["w"], rtol=0, atol=1e-15, err_msg=case["note"])
+
+
+def _sigmoid_f32(logits):
+    """fp32 rounding of the fp64 logistic function (scipy's expit)."""
+    from scipy.special import expit
+    return expit(logits.astype(np.float64)).astype(np.float32)
+
+
+def _unique_top_set(keys, allowed, k):
+    """The unique k-subset of allowed ids preceding every other allowed id in
+    the total order of the keys (tuples, smaller first): brute force."""
+    ids = [e for e in range(len(keys)) if allowed[e]]
+    found = [s for s in itertools.combinations(ids, k)
+             if max(keys[e] for e in s) < min((keys[e] for e in ids if e not in s), default=(9, 0, 0))]
+    assert len(found) == 1
+    return set(found[0])
+
+
+@pytest.mark.parametrize("E,k,n_group,topk_group", [(8, 2, 4, 2), (12, 3, 4, 2), (12, 4, 3, 1), (10, 3, 5, 3),
+                                                    (12, 2, 12, 3), (9, 3, 0, 0)])
+def test_route_sigmoid_grouped_brute_force(oracle_mod, E, k, n_group, topk_group):
+    """Kept groups and selected experts by subset enumeration, on tie-heavy
+    rows (quantised logits and biases) with NaN and infinities."""
+    rng = np.random.default_rng(E * 1000 + k * 10 + n_group)
+    rows = []
+    for _ in range(30):
+        rows.append((rng.integers(-2, 3, size=E) * 0.5).astype(np.float32))
+    for _ in range(15):
+        r = rng.standard_normal(E).astype(np.float32)
+        r[rng.integers(0, E, size=2)] = rng.choice(np.array([np.nan, -np.inf, np.inf], np.float32), 2)
+        rows.append(r)
+    logits = np.stack(rows)
+    bias = (rng.integers(-2, 3, size=E) * 0.125).astype(np.float32)
+    idx, w = oracle_mod.route_gated(logits, k, oracle_mod.GATE_SIGMOID, bias, 2.5, n_group, topk_group)
+    s = _sigmoid_f32(logits)
+    c = s + bias
+    gsz = E // n_group if n_group > 1 else E
+    for t in range(len(rows)):
+        keys = [_sort_key(c[t, e], e) for e in range(E)]
+        allowed = [True] * E
+        if n_group > 1:
+            gs = []
+            for q in range(n_group):
+                members = sorted(range(q * gsz, (q + 1) * gsz), key=lambda e: keys[e])
+                top = [c[t, e] for e in members[:2]]
+                gs.append(np.float32(top[0] + top[1]) if len(top) == 2 else top[0])
+            gkeys = [_sort_key(gs[q], q) for q in range(n_group)]
+            kept = _unique_top_set(gkeys, [True] * n_group, topk_group)
+            allowed = [e // gsz in kept for e in range(E)]
+        assert set(idx[t].tolist()) == _unique_top_set(keys, allowed, k)
+        assert [keys[e] for e in idx[t]] == sorted(keys[e] for e in idx[t])
+        sel = s[t, idx[t]].astype(np.float64)
+        if np.isfinite(sel).all() and sel.sum() > 0:
+            np.testing.assert_allclose(w[t], 2.5 * sel / sel.sum(), rtol=1e-15)
+
+
+def test_route_softmax_full_is_library_softmax(oracle_mod):
+    from scipy.special import softmax
+    rng = np.random.default_rng(11)
+    logits = (rng.standard_normal((300, 24)) * 2).astype(np.float32)
+    logits[rng.random((300, 24)) < 0.05] = -np.inf
+    idx, w = oracle_mod.route_gated(logits, 5, oracle_mod.GATE_SOFTMAX)
+    np.testing.assert_array_equal(idx, np.argsort(-logits, axis=1, kind="stable")[:, :5])
+    full = softmax(logits.astype(np.float64), axis=1)
+    np.testing.assert_allclose(w, np.take_along_axis(full, idx, axis=1), rtol=1e-13, atol=1e-300)
+    _, w_all = oracle_mod.route_gated(logits, 24, oracle_mod.GATE_SOFTMAX)
+    np.testing.assert_allclose(w_all.sum(axis=1), 1.0, rtol=1e-13)
+    assert (w.sum(axis=1) < 1.0 + 1e-12).all()
+
+
+def test_route_bias_moves_selection_not_gates(oracle_mod):
+    """A large bias on a cold expert selects it; its gate stays its sigmoid
+    share of the selected scores."""
+    logits = np.array([[2.0, 1.0, -6.0, 0.5]], np.float32)
+    idx, w = oracle_mod.route_gated(logits, 2, oracle_mod.GATE_SIGMOID)
+    assert idx[0].tolist() == [0, 1]
+    bias = np.array([0.0, 0.0, 5.0, 0.0], np.float32)
+    idx, w = oracle_mod.route_gated(logits, 2, oracle_mod.GATE_SIGMOID, bias)
+    assert idx[0].tolist() == [2, 0]
+    s = _sigmoid_f32(logits[0]).astype(np.float64)
+    np.testing.assert_allclose(w[0], [s[2] / (s[2] + s[0]), s[0] / (s[2] + s[0])], rtol=1e-15)
+
+
+def test_route_group_limit_special_cases(oracle_mod):
+    """One group, or keeping every group, is the ungrouped selection."""
+    rng = np.random.default_rng(12)
+    logits = np.round(rng.standard_normal((200, 16)) * 3).astype(np.float32)
+    bias = (rng.integers(-3, 4, size=16) * 0.25).astype(np.float32)
+    ref, wref = oracle_mod.route_gated(logits, 4, oracle_mod.GATE_SIGMOID, bias)
+    for n_group, topk_group in ((1, 1), (4, 4), (16, 16), (2, 2)):
+        idx, w = oracle_mod.route_gated(logits, 4, oracle_mod.GATE_SIGMOID, bias, 1.0, n_group, topk_group)
+        np.testing.assert_array_equal(idx, ref)
+        np.testing.assert_array_equal(w, wref)
+    # softmax gates under a group limit still take their values from the full softmax
+    from scipy.special import softmax
+    idx, w = oracle_mod.route_gated(logits, 4, oracle_mod.GATE_SOFTMAX, None, 1.0, 4, 2)
+    full = softmax(logits.astype(np.float64), axis=1)
+    np.testing.assert_allclose(w, np.take_along_axis(full, idx, axis=1), rtol=1e-13)
+    assert ((idx // 4)[:, :, None] == (idx // 4)[:, None, :]).any(axis=2).all()
+
+
+def test_route_gated_rejects(oracle_mod):
+    logits = np.zeros((2, 8), np.float32)
+    for args in [dict(gate=3), dict(gate=0, bias=np.zeros(8, np.float32)), dict(gate=2, n_group=3, topk_group=1),
+                 dict(gate=2, n_group=4, topk_group=5), dict(gate=2, n_group=4, topk_group=1, k=3)]:
+        k = args.pop("k", 2)
+        with pytest.raises(oracle_mod.OracleError):
+            oracle_mod.route_gated(logits, k, **args)
