@@ -200,12 +200,14 @@ def cpu_baseline(cfg, wl, budget_s: float) -> dict:
     from oracle import oracle
     oracle.lib()
     t0 = time.perf_counter()
-    oracle.forward_tokens(cfg.dims, [0], wl["logits"], wl["x"], wl["local_experts"], wl)
+    gate = dict(gate=cfg.gate, bias=wl.get("gate_bias"), scale=cfg.routed_scale, n_group=cfg.n_group,
+                topk_group=cfg.topk_group)
+    oracle.forward_tokens(cfg.dims, [0], wl["logits"], wl["x"], wl["local_experts"], wl, **gate)
     per_tok = max(time.perf_counter() - t0, 1e-6)
     n = int(max(1, min(cfg.T, budget_s / per_tok)))
     toks = list(range(n))
     t0 = time.perf_counter()
-    oracle.forward_tokens(cfg.dims, toks, wl["logits"], wl["x"], wl["local_experts"], wl)
+    oracle.forward_tokens(cfg.dims, toks, wl["logits"], wl["x"], wl["local_experts"], wl, **gate)
     dt = time.perf_counter() - t0
     return {"value": n / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
             "sample": f"first {n} of {cfg.T} tokens of {cfg.name}: per-token routing + "
@@ -343,7 +345,9 @@ def main(argv=None) -> int:
     weights = {k: dev(wl[k]) for k in ("w_gate", "w_up", "w_down", "sh_gate", "sh_up", "sh_down")
                if k in wl}
     local = None if wl["local_experts"] is None else dev(wl["local_experts"])
-    layer = moe.MoeLayer(d, weights, local)
+    gate_bias = None if wl.get("gate_bias") is None else dev(wl["gate_bias"])
+    gating = moe.gating(gate_bias, cfg.routed_scale, cfg.n_group, cfg.topk_group) if cfg.gated else None
+    layer = moe.MoeLayer(d, weights, local, gating=gating)
     logits, src, x = dev(wl["logits"]), dev(wl["src"]), dev(wl["x"])
     counts = torch.zeros((cfg.S, cfg.E), dtype=torch.int64, device="cuda")
     out = torch.empty((cfg.T, cfg.H), dtype=torch.bfloat16, device="cuda")
@@ -471,7 +475,11 @@ def main(argv=None) -> int:
         "data": "synthetic",
         "config": {"workload": cfg.name, "T": cfg.T, "H": cfg.H, "E": cfg.E, "k": cfg.k, "I": cfg.I,
                    "S": cfg.S, "E_local": cfg.E_local, "n_shared": cfg.n_shared,
-                   "I_shared": cfg.I_shared if cfg.n_shared else 0, "parallelism": "single GPU"},
+                   "I_shared": cfg.I_shared if cfg.n_shared else 0, "parallelism": "single GPU",
+                   **({"router": {"gate": ["softmax_topk", "softmax", "sigmoid"][cfg.gate],
+                                  "routed_scale": cfg.routed_scale, "n_group": cfg.n_group,
+                                  "topk_group": cfg.topk_group, "selection_bias": cfg.gate_bias_std > 0}}
+                      if cfg.gated else {})},
         "roofline": roof,
         "expert_ffn": {"ms": round(ffn_ms, 4), "frac_mfma": round(ffn_frac_mfma, 4),
                        "frac_hbm": round(ffn_frac_hbm, 4)},

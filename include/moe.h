@@ -39,7 +39,7 @@
 extern "C" {
 #endif
 
-#define MOE_ABI_VERSION 1
+#define MOE_ABI_VERSION 2
 
 typedef uint16_t moe_bf16;
 
@@ -67,7 +67,8 @@ enum moe_status {
  *             x_{l,e,g}, Sec. 5.2), 1 <= E_local <= E.
  *   n_shared  always-on shared experts applied to every token (0 = none).
  *   I_shared  intermediate size of each shared expert (ignored if n_shared=0).
- *   flags     must be 0 (reserved for gating variants).
+ *   flags     the router's gate function, a moe_gate value (its parameters
+ *             travel in moe_gating).
  * Kernel limits (MOE_ERR_UNSUPPORTED beyond them): E <= 1024, k <= 32,
  * H, I, I_shared multiples of 8, I_shared a multiple of 64 when n_shared > 1,
  * T*k < 2^31.
@@ -88,6 +89,41 @@ typedef struct moe_weights {
     const moe_bf16 *w_gate, *w_up, *w_down;
     const moe_bf16 *sh_gate, *sh_up, *sh_down;
 } moe_weights;
+
+/*
+ * Gating variants (Sec. 2.1 requires a router that picks each token's top-k
+ * experts; it does not fix the gating function, so three common ones are
+ * offered).  moe_dims.flags selects one:
+ *   MOE_GATE_SOFTMAX_TOPK  the softmax of the k selected logits, renormalised
+ *                          over them (the default; selection on the logits);
+ *   MOE_GATE_SOFTMAX       the softmax over all E logits evaluated at the k
+ *                          selected experts, not renormalised (selection on
+ *                          the logits);
+ *   MOE_GATE_SIGMOID       sigmoid scores s_e = sigma(l_e), evaluated in fp64
+ *                          and rounded to fp32; selection on s_e + bias_e
+ *                          (fp32; the bias moves the selection only), gates
+ *                          s_j / sum of the k selected s.
+ * The moe_gating struct, nullable for no bias, scale 1 and no group limit, adds:
+ *   bias          [E] fp32 device, nullable, MOE_GATE_SIGMOID only.
+ *   routed_scale  every gate is multiplied by it.
+ *   n_group, topk_group  group-limited selection when n_group > 1: the
+ *                 experts form n_group groups of E / n_group consecutive ids;
+ *                 a group's score is the fp32 sum of its two first selection
+ *                 values in selection order (the single value when groups
+ *                 hold one expert); only the topk_group first groups by
+ *                 score (ties to the lower group) stay, and the k experts are
+ *                 chosen among theirs.  Requires E % n_group == 0,
+ *                 n_group <= 64, 1 <= topk_group <= n_group and
+ *                 k <= topk_group * E / n_group.
+ * Selection always orders by value descending, lower index first, NaN last.
+ */
+enum moe_gate { MOE_GATE_SOFTMAX_TOPK = 0, MOE_GATE_SOFTMAX = 1, MOE_GATE_SIGMOID = 2 };
+
+typedef struct moe_gating {
+    const float *bias;
+    float routed_scale;
+    int32_t n_group, topk_group;
+} moe_gating;
 
 /* Which entry point a workspace size refers to. */
 enum moe_entry { MOE_ENTRY_PERMUTE = 1, MOE_ENTRY_EXPERT_FFN = 2, MOE_ENTRY_FORWARD = 3 };
@@ -144,17 +180,20 @@ int moe_validate(const moe_dims *dims, int entry, size_t ws_bytes);
 
 /*
  * Top-k gating (Sec. 2.1: the router selects the top-k experts of each token).
- *   logits    [T][E] fp32, row-major, any bias already added.
+ *   gating    nullable host struct: the parameters of the gate function that
+ *             dims->flags selects (see moe_gating).
+ *   logits    [T][E] fp32, row-major.
  *   topk_idx  [T][k] int32 out: the k selected experts of each token, ordered
- *             by logit descending; equal logits (-0.0 equals +0.0) go to the
- *             lower expert index; NaN ranks below every number.
- *   topk_w    [T][k] fp32 out: gates, the softmax of the selected logits
- *             renormalised over the k selected (NaN when the largest selected
- *             logit is not finite).
- * Uses T, E, k.  T = 0 is a no-op.
+ *             by selection value descending; equal values (-0.0 equals +0.0)
+ *             go to the lower expert index; NaN ranks below every number.
+ *   topk_w    [T][k] fp32 out: the gates (with the default gate function:
+ *             the softmax of the selected logits renormalised over the k
+ *             selected, NaN when the largest selected logit is not finite).
+ * Uses T, E, k, flags.  T = 0 is a no-op.
  */
-int moe_route(const moe_dims *dims, const float *logits, int32_t *topk_idx,
-              float *topk_w, void *stream);
+int moe_route(const moe_dims *dims, const moe_gating *gating,
+              const float *logits, int32_t *topk_idx, float *topk_w,
+              void *stream);
 
 /*
  * Source-aware routing statistics (Sec. 5.1: the source x expert matrix
@@ -234,6 +273,7 @@ int moe_combine(const moe_dims *dims, const moe_bf16 *y_perm,
 /*
  * The whole layer: moe_route (+ moe_route_stats) -> moe_permute ->
  * moe_expert_ffn -> moe_combine, with the intermediates in the workspace.
+ *   gating as in moe_route;
  *   logits [T][E] fp32; src [T] int32 (nullable when counts is NULL);
  *   x [T][H] bf16; local_experts as in moe_permute; weights as in
  *   moe_expert_ffn;
@@ -244,7 +284,8 @@ int moe_combine(const moe_dims *dims, const moe_bf16 *y_perm,
  *   taps   nullable host struct of optional extra outputs and events;
  *   ws     MOE_ENTRY_FORWARD workspace.
  */
-int moe_forward(const moe_dims *dims, const float *logits, const int32_t *src,
+int moe_forward(const moe_dims *dims, const moe_gating *gating,
+                const float *logits, const int32_t *src,
                 const moe_bf16 *x, const int32_t *local_experts,
                 const moe_weights *weights, int64_t *counts, moe_bf16 *out,
                 const moe_taps *taps, void *ws, size_t ws_bytes, void *stream);

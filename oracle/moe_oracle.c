@@ -523,7 +523,11 @@ int oracle_combine(int T, int k, int H, int R, const uint16_t *y_perm,
  * over q ascending.  Tokens whose experts are all remote receive only the
  * shared part (zero without shared experts).
  *
- * dims = {T, H, E, k, I, S, E_local, n_shared, I_shared}; routed weights are
+ * The routing is oracle_route_gated with gate = dims[9] and the gating
+ * parameters given (gate 0 with no bias, scale 1 and no group limit is
+ * oracle_route).
+ *
+ * dims = {T, H, E, k, I, S, E_local, n_shared, I_shared, gate}; routed weights are
  * stacked by local slot, shared ones as [n_shared][I_shared][H] (gate, up)
  * and [n_shared][H][I_shared] (down).
  *
@@ -536,10 +540,12 @@ int oracle_forward_tokens(const int32_t *dims, int n_tok, const int32_t *tokens,
                           const int32_t *local_experts, const uint16_t *w_gate,
                           const uint16_t *w_up, const uint16_t *w_down,
                           const uint16_t *sh_gate, const uint16_t *sh_up,
-                          const uint16_t *sh_down, double *out)
+                          const uint16_t *sh_down, const float *gate_bias,
+                          double gate_scale, int n_group, int topk_group,
+                          double *out)
 {
     int T = dims[0], H = dims[1], E = dims[2], k = dims[3], I = dims[4];
-    int E_local = dims[6], n_sh = dims[7], I_sh = dims[8];
+    int E_local = dims[6], n_sh = dims[7], I_sh = dims[8], gate = dims[9];
     if (T < 0 || H < 1 || E < 1 || k < 1 || k > E || I < 1 || E_local < 1 ||
         E_local > E || n_sh < 0 || (n_sh > 0 && I_sh < 1) || n_tok < 0)
         return ORACLE_ERR_DIMS;
@@ -575,7 +581,8 @@ int oracle_forward_tokens(const int32_t *dims, int n_tok, const int32_t *tokens,
         }
         const uint16_t *xt = x + (size_t)t * H;
         double *o = out + (size_t)n * H;
-        rc = oracle_route(1, E, k, logits + (size_t)t * E, idx, w);
+        rc = oracle_route_gated(1, E, k, gate, logits + (size_t)t * E, gate_bias,
+                                gate_scale, n_group, topk_group, idx, w);
         if (rc != ORACLE_OK)
             goto done;
         for (int c = 0; c < H; ++c)

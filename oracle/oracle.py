@@ -61,7 +61,7 @@ def lib():
         L.oracle_ffn_rows.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int, _i32p, _u16p, _u16p, _u16p, _u16p, _f64p]
         L.oracle_combine.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int, _u16p, _i32p, _f32p, _vp, _f64p]
         L.oracle_forward_tokens.argtypes = [_i32p, C.c_int, _i32p, _f32p, _u16p, _vp, _u16p, _u16p, _u16p,
-                                            _vp, _vp, _vp, _f64p]
+                                            _vp, _vp, _vp, _vp, C.c_double, C.c_int, C.c_int, _f64p]
         L.oracle_place_objective.argtypes = [C.c_int] * 4 + [_i64p, _vp, _f64p, _vp, C.c_double, _i32p,
                                                              _i32p, _f64p]
         L.oracle_place_greedy.argtypes = [C.c_int] * 4 + [_i64p, _vp, _f64p, _vp, C.c_double, _i32p, _i32p,
@@ -207,21 +207,24 @@ def combine(y_perm, inv_pos, topk_w, y_shared=None, H=None) -> np.ndarray:
     return out[:T]
 
 
-def forward_tokens(dims: dict, tokens, logits, x, local_experts, weights: dict) -> np.ndarray:
+def forward_tokens(dims: dict, tokens, logits, x, local_experts, weights: dict, gate: int = 0, bias=None,
+                   scale: float = 1.0, n_group: int = 0, topk_group: int = 0) -> np.ndarray:
     """Layer output [len(tokens), H] in fp64 for the listed tokens, from the definition."""
     d = np.array([dims["T"], dims["H"], dims["E"], dims["k"], dims["I"], dims["S"],
-                  dims["E_local"], dims.get("n_shared", 0), dims.get("I_shared", 0)], np.int32)
+                  dims["E_local"], dims.get("n_shared", 0), dims.get("I_shared", 0), gate], np.int32)
     tokens = _c(tokens, np.int32)
     loc = None if local_experts is None else _c(local_experts, np.int32)
     n_sh = dims.get("n_shared", 0)
     shg = _c(weights["sh_gate"], np.uint16) if n_sh else None
     shu = _c(weights["sh_up"], np.uint16) if n_sh else None
     shd = _c(weights["sh_down"], np.uint16) if n_sh else None
+    b = None if bias is None else _c(bias, np.float32)
     out = np.empty((max(len(tokens), 1), dims["H"]), np.float64)
     _check(lib().oracle_forward_tokens(d, len(tokens), tokens, _c(logits, np.float32), _c(x, np.uint16),
                                        _ptr(loc), _c(weights["w_gate"], np.uint16),
                                        _c(weights["w_up"], np.uint16), _c(weights["w_down"], np.uint16),
-                                       _ptr(shg), _ptr(shu), _ptr(shd), out), "oracle_forward_tokens")
+                                       _ptr(shg), _ptr(shu), _ptr(shd), _ptr(b), float(scale), n_group,
+                                       topk_group, out), "oracle_forward_tokens")
     return out[: len(tokens)]
 
 

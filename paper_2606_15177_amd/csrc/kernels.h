@@ -9,12 +9,22 @@
 namespace moe {
 
 // ---- route.hip -------------------------------------------------------------
+// Gating variant of the router (see moe.h): gate 0 softmax over the picks,
+// 1 full softmax, 2 sigmoid scores; bias (selection only, gate 2), scale,
+// and a group limit when n_group > 1 (n_group <= 64).
+struct RouteGating {
+  int gate;
+  const float* bias;
+  float scale;
+  int n_group, topk_group;
+};
 // Top-k selection + gates; when counts != nullptr also accumulates the
 // source x expert counts (and sets expert_load if non-null, which must have
-// been zeroed on the stream before).
+// been zeroed on the stream before).  gating == nullptr: softmax over the
+// picks, unscaled, no group limit.
 hipError_t launch_route(int T, int E, int k, const float* logits, int32_t* topk_idx,
                         float* topk_w, const int32_t* src, int S, int64_t* counts,
-                        int32_t* expert_load, hipStream_t st);
+                        int32_t* expert_load, const RouteGating* gating, hipStream_t st);
 // Counts from (src, topk_idx); expert_load as above.
 hipError_t launch_route_stats(int T, int k, int S, int E, const int32_t* src,
                               const int32_t* topk_idx, int64_t* counts, int32_t* expert_load,

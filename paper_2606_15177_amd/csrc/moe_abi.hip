@@ -22,13 +22,32 @@ int check_dims(const moe_dims* d) {
       d->E_local < 1 || d->E_local > d->E || d->n_shared < 0 ||
       (d->n_shared > 0 && d->I_shared < 1))
     return MOE_ERR_DIMS;
-  if (d->flags != 0) return MOE_ERR_UNSUPPORTED;
+  if (d->flags < MOE_GATE_SOFTMAX_TOPK || d->flags > MOE_GATE_SIGMOID) return MOE_ERR_UNSUPPORTED;
   if (d->E > 1024 || d->k > 32) return MOE_ERR_UNSUPPORTED;
   if (d->H % 8 != 0 || d->I % 8 != 0 || (d->n_shared > 0 && d->I_shared % 8 != 0))
     return MOE_ERR_UNSUPPORTED;
   if (static_cast<int64_t>(d->T) * d->k > kIntMax || static_cast<int64_t>(d->S) * d->E > kIntMax ||
       static_cast<int64_t>(d->n_shared) * std::max(d->I_shared, 0) > kIntMax)
     return MOE_ERR_UNSUPPORTED;
+  return MOE_OK;
+}
+
+// The router's gating variant: dims->flags picks the gate function, g (may be
+// null) carries its parameters.
+int gating_ok(const moe_dims* d, const moe_gating* g, moe::RouteGating* out) {
+  *out = moe::RouteGating{d->flags, nullptr, 1.0f, 0, 0};
+  if (g == nullptr) return MOE_OK;
+  if (g->bias && d->flags != MOE_GATE_SIGMOID) return MOE_ERR_DIMS;
+  if (g->bias && (reinterpret_cast<uintptr_t>(g->bias) & 3u) != 0) return MOE_ERR_ALIGN;
+  if (g->n_group > 1) {
+    if (g->n_group > 64) return MOE_ERR_UNSUPPORTED;
+    if (d->E % g->n_group != 0 || g->topk_group < 1 || g->topk_group > g->n_group ||
+        d->k > g->topk_group * (d->E / g->n_group))
+      return MOE_ERR_DIMS;
+  } else if (g->n_group < 0) {
+    return MOE_ERR_DIMS;
+  }
+  *out = moe::RouteGating{d->flags, g->bias, g->routed_scale, g->n_group, g->topk_group};
   return MOE_OK;
 }
 
@@ -217,13 +236,16 @@ int moe_validate(const moe_dims* d, int entry, size_t ws_bytes) {
   return MOE_OK;
 }
 
-int moe_route(const moe_dims* d, const float* logits, int32_t* topk_idx, float* topk_w,
-              void* stream) {
+int moe_route(const moe_dims* d, const moe_gating* gating, const float* logits, int32_t* topk_idx,
+              float* topk_w, void* stream) {
   int s = check_dims(d);
+  if (s != MOE_OK) return s;
+  moe::RouteGating rg;
+  s = gating_ok(d, gating, &rg);
   if (s != MOE_OK) return s;
   if (d->T > 0 && (!logits || !topk_idx || !topk_w)) return MOE_ERR_NULL;
   return status(moe::launch_route(d->T, d->E, d->k, logits, topk_idx, topk_w, nullptr, d->S,
-                                  nullptr, nullptr, static_cast<hipStream_t>(stream)));
+                                  nullptr, nullptr, &rg, static_cast<hipStream_t>(stream)));
 }
 
 int moe_route_stats(const moe_dims* d, const int32_t* src, const int32_t* topk_idx,
@@ -289,10 +311,13 @@ int moe_combine(const moe_dims* d, const moe_bf16* y_perm, const int32_t* inv_po
                                     static_cast<hipStream_t>(stream)));
 }
 
-int moe_forward(const moe_dims* d, const float* logits, const int32_t* src, const moe_bf16* x,
-                const int32_t* local_experts, const moe_weights* w, int64_t* counts,
+int moe_forward(const moe_dims* d, const moe_gating* gating, const float* logits, const int32_t* src,
+                const moe_bf16* x, const int32_t* local_experts, const moe_weights* w, int64_t* counts,
                 moe_bf16* out, const moe_taps* taps, void* ws, size_t ws_bytes, void* stream) {
   int s = check_dims(d);
+  if (s != MOE_OK) return s;
+  moe::RouteGating rg;
+  s = gating_ok(d, gating, &rg);
   if (s != MOE_OK) return s;
   if (!local_experts && d->E_local != d->E) return MOE_ERR_DIMS;
   s = weights_ok(d, w);
@@ -319,7 +344,7 @@ int moe_forward(const moe_dims* d, const float* logits, const int32_t* src, cons
     if (e != hipSuccess) return MOE_ERR_DEVICE;
   }
   e = moe::launch_route(d->T, d->E, d->k, logits, topk_idx, topk_w, counts ? src : nullptr, d->S,
-                        counts, counts ? expert_load : nullptr, st);
+                        counts, counts ? expert_load : nullptr, &rg, st);
   if (e != hipSuccess) return MOE_ERR_DEVICE;
   record(taps, 2 * MOE_STAGE_ROUTE + 1, st);
 

@@ -10,6 +10,15 @@
 // lane j of the group keeps the j-th pick, then the group computes the gates,
 // the softmax of the picked logits renormalised over the k picks.
 //
+// Gating variants (the EXT instantiations): the selection value may instead be
+// a sigmoid score s = sigma(l), evaluated in fp64 and rounded to fp32, plus a
+// selection-only bias; gates may be the full softmax over all E logits or the
+// picked sigmoid scores renormalised; all gates may be scaled.  Under a group
+// limit the token's selection values are staged in LDS, lane q of the group
+// sums the two first values of expert group q, topk_group rounds of a max
+// over those sums keep groups, and the experts of the other groups drop out of
+// the selection (key 0, below every kept expert, NaN included).
+//
 // Statistics (Sec. 5.1, the matrices A_{l,s,e} and B_{l,e}): each block
 // counts its pairs into an S x E int32 histogram in LDS and flushes the
 // non-zero bins with one 64-bit atomic add each.  Integer atomics make the
@@ -59,37 +68,123 @@ __device__ __forceinline__ void flush_hist(const int* hist, int bins, int E,
   }
 }
 
-template <int G, int V>
-__global__ __launch_bounds__(kBlock) void route_kernel(
-    int T, int E, int k, int tokens_per_block, const float* __restrict__ logits,
-    int32_t* __restrict__ topk_idx, float* __restrict__ topk_w, const int32_t* __restrict__ src,
-    int S, unsigned long long* __restrict__ counts, int32_t* __restrict__ expert_load,
-    int lds_bins) {
+struct RouteKernelArgs {
+  int T, E, k, tokens_per_block;
+  const float* logits;
+  int32_t* topk_idx;
+  float* topk_w;
+  const int32_t* src;
+  int S;
+  unsigned long long* counts;
+  int32_t* expert_load;
+  int lds_bins;          // S*E histogram bins in LDS (0: global atomics)
+  // gating variant
+  int gate;              // 0 softmax over the picks, 1 full softmax, 2 sigmoid
+  const float* bias;     // [E] selection-only bias (gate 2), nullable
+  float scale;           // gates are multiplied by this
+  int n_group, topk_group;  // group limit when n_group > 1
+};
+
+__device__ __forceinline__ float sigmoid_score(float l) {
+  return static_cast<float>(1.0 / (1.0 + exp(-static_cast<double>(l))));
+}
+
+template <int G>
+__device__ __forceinline__ uint64_t group_max64(uint64_t v) {
+#pragma unroll
+  for (int off = G / 2; off > 0; off >>= 1)
+    v = umax64(v, __shfl_xor(static_cast<unsigned long long>(v), off, G));
+  return v;
+}
+
+template <int G>
+__device__ __forceinline__ float group_sum(float v) {
+#pragma unroll
+  for (int off = G / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, G);
+  return v;
+}
+
+template <int G, int V, bool EXT>
+__global__ __launch_bounds__(kBlock) void route_kernel(RouteKernelArgs a) {
   extern __shared__ int hist[];
   constexpr int kGroups = kBlock / G;
-  const bool stats = counts != nullptr;
-  const bool use_lds = lds_bins > 0;
+  const int T = a.T, E = a.E, k = a.k;
+  const bool stats = a.counts != nullptr;
+  const bool use_lds = a.lds_bins > 0;
   const int tid = threadIdx.x;
   const int gl = tid & (G - 1);
   const int group = tid / G;
+  // group-limit staging: one row of E selection values per token group,
+  // after the histogram
+  float* cval = reinterpret_cast<float*>(hist + a.lds_bins) + group * E;
+  const bool grouped = EXT && a.n_group > 1;
+  const int gsz = grouped ? E / a.n_group : E;
   if (stats && use_lds) {
-    for (int b = tid; b < lds_bins; b += kBlock) hist[b] = 0;
+    for (int b = tid; b < a.lds_bins; b += kBlock) hist[b] = 0;
     __syncthreads();
   }
-  const int t0 = blockIdx.x * tokens_per_block;
-  const int t1 = min(T, t0 + tokens_per_block);
+  const int t0 = blockIdx.x * a.tokens_per_block;
+  const int t1 = min(T, t0 + a.tokens_per_block);
   for (int base = t0; base < t1; base += kGroups) {
     const int t = base + group;
     const bool valid = t < t1;
     uint64_t key[V];
+    float lg[V];
 #pragma unroll
     for (int v = 0; v < V; ++v) {
       const int e = gl + G * v;
       key[v] = 0;
+      lg[v] = __builtin_nanf("");
       if (valid && e < E) {
-        const float f = logits[static_cast<size_t>(t) * E + e];
-        key[v] = (static_cast<uint64_t>(order_key(f)) << 32) | static_cast<uint32_t>(~e);
+        const float f = a.logits[static_cast<size_t>(t) * E + e];
+        lg[v] = f;
+        float c = f;
+        if (EXT && a.gate == 2) {
+          c = sigmoid_score(f);
+          if (a.bias) c = c + a.bias[e];
+        }
+        if (grouped) cval[e] = c;
+        key[v] = (static_cast<uint64_t>(order_key(c)) << 32) | static_cast<uint32_t>(~e);
       }
+    }
+    if (grouped) {
+      // the group's lanes share this wave: a block-wide barrier is not needed
+      // between its LDS writes and reads, only the LDS wait
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+      __builtin_amdgcn_wave_barrier();
+      // lane q: the two first selection values of expert group q, then their sum
+      uint64_t gkey = 0;
+      if (valid && gl < a.n_group) {
+        uint64_t k1 = 0, k2 = 0;
+        for (int e = gl * gsz; e < (gl + 1) * gsz; ++e) {
+          const uint64_t ke = (static_cast<uint64_t>(order_key(cval[e])) << 32) | static_cast<uint32_t>(~e);
+          if (ke > k1) {
+            k2 = k1;
+            k1 = ke;
+          } else if (ke > k2) {
+            k2 = ke;
+          }
+        }
+        const float c1 = cval[~static_cast<uint32_t>(k1)];
+        const float gs = gsz > 1 ? c1 + cval[~static_cast<uint32_t>(k2)] : c1;
+        gkey = (static_cast<uint64_t>(order_key(gs)) << 32) | static_cast<uint32_t>(~gl);
+      }
+      uint64_t kept = 0;   // bit q: group q stays
+      for (int r = 0; r < a.topk_group; ++r) {
+        const uint64_t best = group_max64<G>(gkey);
+        if (best == 0) break;   // a token group past the batch end
+        const int q = static_cast<int>(~static_cast<uint32_t>(best));
+        kept |= 1ull << q;
+        if (gl == q) gkey = 0;
+      }
+#pragma unroll
+      for (int v = 0; v < V; ++v) {
+        const int e = gl + G * v;
+        if (e < E && !((kept >> (e / gsz)) & 1ull)) key[v] = 0;
+      }
+      // the next token's writes must not overtake this token's reads
+      __builtin_amdgcn_s_waitcnt(0xc07f);
+      __builtin_amdgcn_wave_barrier();
     }
     uint32_t my_key = 0;
     int my_e = 0;
@@ -97,9 +192,7 @@ __global__ __launch_bounds__(kBlock) void route_kernel(
       uint64_t best = key[0];
 #pragma unroll
       for (int v = 1; v < V; ++v) best = umax64(best, key[v]);
-#pragma unroll
-      for (int off = G / 2; off > 0; off >>= 1)
-        best = umax64(best, __shfl_xor(static_cast<unsigned long long>(best), off, G));
+      best = group_max64<G>(best);
       const int e = static_cast<int>(~static_cast<uint32_t>(best));
 #pragma unroll
       for (int v = 0; v < V; ++v)
@@ -109,22 +202,45 @@ __global__ __launch_bounds__(kBlock) void route_kernel(
         my_e = e;
       }
     }
-    const float val = key_value(my_key);
-    const float m = __shfl(val, 0, G);
-    const float ex = (gl < k) ? expf(val - m) : 0.0f;
-    float sum = ex;
+    float wgt;
+    if (!EXT || a.gate == 0) {
+      const float val = key_value(my_key);
+      const float m = __shfl(val, 0, G);
+      const float ex = (gl < k) ? expf(val - m) : 0.0f;
+      wgt = ex / group_sum<G>(ex);
+    } else if (a.gate == 1) {
+      // softmax over all E logits: M is the largest logit that is a number,
+      // then every exp(l - M) is summed
+      uint32_t mk = 0;
 #pragma unroll
-    for (int off = G / 2; off > 0; off >>= 1) sum += __shfl_xor(sum, off, G);
+      for (int v = 0; v < V; ++v)
+        if (lg[v] == lg[v]) mk = max(mk, order_key(lg[v]));
+#pragma unroll
+      for (int off = G / 2; off > 0; off >>= 1) mk = max(mk, static_cast<uint32_t>(__shfl_xor(static_cast<int>(mk), off, G)));
+      const float M = mk ? key_value(mk) : __builtin_nanf("");
+      float part = 0.0f;
+#pragma unroll
+      for (int v = 0; v < V; ++v)
+        if (gl + G * v < E) part += expf(lg[v] - M);
+      const float sum = group_sum<G>(part);
+      const float lj = (valid && gl < k) ? a.logits[static_cast<size_t>(t) * E + my_e] : 0.0f;
+      wgt = expf(lj - M) / sum;
+    } else {
+      // picked sigmoid scores renormalised over the picks
+      const float sj = (valid && gl < k) ? sigmoid_score(a.logits[static_cast<size_t>(t) * E + my_e]) : 0.0f;
+      wgt = sj / group_sum<G>(sj);
+    }
+    if (EXT) wgt *= a.scale;
     if (valid && gl < k) {
       const size_t o = static_cast<size_t>(t) * k + gl;
-      topk_idx[o] = my_e;
-      topk_w[o] = ex / sum;
-      if (stats) count_pair(src[t], my_e, S, E, use_lds, hist, counts, expert_load);
+      a.topk_idx[o] = my_e;
+      a.topk_w[o] = wgt;
+      if (stats) count_pair(a.src[t], my_e, a.S, E, use_lds, hist, a.counts, a.expert_load);
     }
   }
   if (stats && use_lds) {
     __syncthreads();
-    flush_hist(hist, lds_bins, E, counts, expert_load);
+    flush_hist(hist, a.lds_bins, E, a.counts, a.expert_load);
   }
 }
 
@@ -156,41 +272,70 @@ __global__ void fill_i32_kernel(int32_t* p, int n, int32_t value) {
   if (i < n) p[i] = value;
 }
 
-template <int G, int V>
-hipError_t launch_route_gv(int T, int E, int k, const float* logits, int32_t* topk_idx,
-                           float* topk_w, const int32_t* src, int S, int64_t* counts,
-                           int32_t* expert_load, hipStream_t st) {
+template <int G, int V, bool EXT>
+hipError_t launch_route_gv(const RouteKernelArgs& in, hipStream_t st) {
   constexpr int kGroups = kBlock / G;
+  RouteKernelArgs a = in;
   // 4 tokens per group and block keeps the histogram flush amortised while
   // leaving enough blocks to fill the chip at the prefill sizes.
-  const int tokens_per_block = kGroups * 4;
-  const int blocks = ceil_div(T, tokens_per_block);
-  const int bins = (counts && S * E <= kLdsBinsMax) ? S * E : 0;
-  hipLaunchKernelGGL((route_kernel<G, V>), dim3(blocks), dim3(kBlock), bins * sizeof(int), st, T,
-                     E, k, tokens_per_block, logits, topk_idx, topk_w, src, S,
-                     reinterpret_cast<unsigned long long*>(counts), expert_load, bins);
+  a.tokens_per_block = kGroups * 4;
+  const int blocks = ceil_div(a.T, a.tokens_per_block);
+  a.lds_bins = (a.counts && a.S * a.E <= kLdsBinsMax) ? a.S * a.E : 0;
+  const size_t lds = a.lds_bins * sizeof(int) + ((EXT && a.n_group > 1) ? sizeof(float) * kGroups * a.E : 0);
+  if (EXT) {
+    static bool attr_set = false;
+    if (!attr_set) {
+      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&route_kernel<G, V, EXT>),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+      if (e != hipSuccess) return e;
+      attr_set = true;
+    }
+  }
+  hipLaunchKernelGGL((route_kernel<G, V, EXT>), dim3(blocks), dim3(kBlock), lds, st, a);
   return hipGetLastError();
+}
+
+template <bool EXT>
+hipError_t launch_route_ext(const RouteKernelArgs& a, hipStream_t st) {
+  const int E = a.E;
+  if (E <= 2) return launch_route_gv<2, 1, EXT>(a, st);
+  if (E <= 4) return launch_route_gv<4, 1, EXT>(a, st);
+  if (E <= 8) return launch_route_gv<8, 1, EXT>(a, st);
+  if (E <= 16) return launch_route_gv<16, 1, EXT>(a, st);
+  if (E <= 32) return launch_route_gv<32, 1, EXT>(a, st);
+  if (E <= 64) return launch_route_gv<64, 1, EXT>(a, st);
+  if (E <= 128) return launch_route_gv<64, 2, EXT>(a, st);
+  if (E <= 256) return launch_route_gv<64, 4, EXT>(a, st);
+  if (E <= 512) return launch_route_gv<64, 8, EXT>(a, st);
+  return launch_route_gv<64, 16, EXT>(a, st);
 }
 
 }  // namespace
 
 hipError_t launch_route(int T, int E, int k, const float* logits, int32_t* topk_idx,
                         float* topk_w, const int32_t* src, int S, int64_t* counts,
-                        int32_t* expert_load, hipStream_t st) {
+                        int32_t* expert_load, const RouteGating* gating, hipStream_t st) {
   if (T == 0) return hipSuccess;
-#define MOE_ROUTE(G, V) \
-  return launch_route_gv<G, V>(T, E, k, logits, topk_idx, topk_w, src, S, counts, expert_load, st)
-  if (E <= 2) MOE_ROUTE(2, 1);
-  if (E <= 4) MOE_ROUTE(4, 1);
-  if (E <= 8) MOE_ROUTE(8, 1);
-  if (E <= 16) MOE_ROUTE(16, 1);
-  if (E <= 32) MOE_ROUTE(32, 1);
-  if (E <= 64) MOE_ROUTE(64, 1);
-  if (E <= 128) MOE_ROUTE(64, 2);
-  if (E <= 256) MOE_ROUTE(64, 4);
-  if (E <= 512) MOE_ROUTE(64, 8);
-  MOE_ROUTE(64, 16);
-#undef MOE_ROUTE
+  RouteKernelArgs a{};
+  a.T = T;
+  a.E = E;
+  a.k = k;
+  a.logits = logits;
+  a.topk_idx = topk_idx;
+  a.topk_w = topk_w;
+  a.src = src;
+  a.S = S;
+  a.counts = reinterpret_cast<unsigned long long*>(counts);
+  a.expert_load = expert_load;
+  a.scale = 1.0f;
+  const bool ext = gating && (gating->gate != 0 || gating->bias || gating->n_group > 1 || gating->scale != 1.0f);
+  if (!ext) return launch_route_ext<false>(a, st);
+  a.gate = gating->gate;
+  a.bias = gating->bias;
+  a.scale = gating->scale;
+  a.n_group = gating->n_group;
+  a.topk_group = gating->topk_group;
+  return launch_route_ext<true>(a, st);
 }
 
 hipError_t launch_route_stats(int T, int k, int S, int E, const int32_t* src,

@@ -20,6 +20,7 @@ HEADER = os.path.join(os.path.dirname(_HERE), "include", "moe.h")
 MOE_OK, MOE_ERR_NULL, MOE_ERR_DIMS, MOE_ERR_UNSUPPORTED = 0, -1, -2, -3
 MOE_ERR_WORKSPACE, MOE_ERR_DEVICE, MOE_ERR_ALIGN = -4, -5, -6
 ENTRY_PERMUTE, ENTRY_EXPERT_FFN, ENTRY_FORWARD = 1, 2, 3
+GATE_SOFTMAX_TOPK, GATE_SOFTMAX, GATE_SIGMOID = 0, 1, 2   # moe_dims.flags
 STAGES = ("route", "permute", "ffn_up", "ffn_down", "combine")
 
 
@@ -30,6 +31,11 @@ class MoeDims(C.Structure):
 
 class MoeWeights(C.Structure):
     _fields_ = [(n, C.c_void_p) for n in ("w_gate", "w_up", "w_down", "sh_gate", "sh_up", "sh_down")]
+
+
+class MoeGating(C.Structure):
+    _fields_ = [("bias", C.c_void_p), ("routed_scale", C.c_float), ("n_group", C.c_int32),
+                ("topk_group", C.c_int32)]
 
 
 class MoeTaps(C.Structure):
@@ -65,13 +71,13 @@ def _load() -> C.CDLL:
         "moe_strerror": ([i32], C.c_char_p),
         "moe_workspace_bytes": ([dp, i32], sz),
         "moe_validate": ([dp, i32, sz], i32),
-        "moe_route": ([dp, vp, vp, vp, vp], i32),
+        "moe_route": ([dp, C.POINTER(MoeGating), vp, vp, vp, vp], i32),
         "moe_route_stats": ([dp, vp, vp, vp, vp, vp], i32),
         "moe_permute": ([dp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp], i32),
         "moe_expert_ffn": ([dp, vp, vp, C.POINTER(MoeWeights), vp, vp, vp, vp, sz, vp], i32),
         "moe_combine": ([dp, vp, vp, vp, vp, vp, vp], i32),
-        "moe_forward": ([dp, vp, vp, vp, vp, C.POINTER(MoeWeights), vp, vp, C.POINTER(MoeTaps),
-                         vp, sz, vp], i32),
+        "moe_forward": ([dp, C.POINTER(MoeGating), vp, vp, vp, vp, C.POINTER(MoeWeights), vp, vp,
+                         C.POINTER(MoeTaps), vp, sz, vp], i32),
         "moe_place_slots": ([C.POINTER(MoePlaceDims), vp], sz),
         "moe_place_experts": ([C.POINTER(MoePlaceDims), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp], i32),
         "moe_window_stats": ([C.POINTER(MoeWindowDims), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp], i32),
@@ -108,6 +114,7 @@ def dims(T, H, E, k, I, S, E_local, n_shared=0, I_shared=0, flags=0) -> MoeDims:
 
 def dims_of(cfg, **override) -> MoeDims:
     d = dict(cfg.dims)
+    d["flags"] = getattr(cfg, "gate", 0)
     d.update(override)
     return dims(**d)
 
@@ -157,9 +164,19 @@ def workspace(d: MoeDims, entry: int, device="cuda") -> torch.Tensor:
     return torch.empty(max(workspace_bytes(d, entry), 1), dtype=torch.uint8, device=device)
 
 
-def route(d, logits, topk_idx, topk_w, stream=None):
-    _check(_lib.moe_route(C.byref(d), _ptr(logits, _F32), _ptr(topk_idx, _I32), _ptr(topk_w, _F32),
-                          _stream(stream)), "moe_route")
+def gating(bias=None, routed_scale=1.0, n_group=0, topk_group=0) -> MoeGating:
+    """Parameters of the gate function that moe_dims.flags selects; bias is a
+    device fp32 [E] tensor (sigmoid gates only)."""
+    return MoeGating(_ptr(bias, _F32), float(routed_scale), int(n_group), int(topk_group))
+
+
+def _gating_ref(g):
+    return None if g is None else C.byref(g)
+
+
+def route(d, logits, topk_idx, topk_w, stream=None, gating=None):
+    _check(_lib.moe_route(C.byref(d), _gating_ref(gating), _ptr(logits, _F32), _ptr(topk_idx, _I32),
+                          _ptr(topk_w, _F32), _stream(stream)), "moe_route")
 
 
 def route_stats(d, src, topk_idx, counts, expert_load=None, stream=None):
@@ -198,9 +215,9 @@ def make_taps(topk_idx=None, topk_w=None, expert_load=None, offsets=None, perm_t
     return t
 
 
-def forward(d, logits, src, x, local_experts, weights, counts, out, ws, taps=None, stream=None):
+def forward(d, logits, src, x, local_experts, weights, counts, out, ws, taps=None, stream=None, gating=None):
     w = weights if isinstance(weights, MoeWeights) else make_weights(weights)
-    _check(_lib.moe_forward(C.byref(d), _ptr(logits, _F32), _ptr(src, _I32), _ptr(x, _BF16),
+    _check(_lib.moe_forward(C.byref(d), _gating_ref(gating), _ptr(logits, _F32), _ptr(src, _I32), _ptr(x, _BF16),
                             _ptr(local_experts, _I32), C.byref(w), _ptr(counts, _I64),
                             _ptr(out, _BF16), None if taps is None else C.byref(taps), _ptr(ws),
                             0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)),
@@ -254,8 +271,9 @@ class MoeLayer:
     calls moe_forward.  ``counts`` (int64 [S, E]) is the caller's source x
     expert matrix for this layer, accumulated by every call."""
 
-    def __init__(self, d: MoeDims, weights: dict, local_experts=None, device="cuda"):
+    def __init__(self, d: MoeDims, weights: dict, local_experts=None, device="cuda", gating=None):
         self.d = d
+        self.gating = gating   # MoeGating for the gate function d.flags selects (None: defaults)
         self.weights = {k: v for k, v in weights.items() if v is not None}
         self.local_experts = local_experts
         self._w = make_weights(self.weights)
@@ -265,5 +283,6 @@ class MoeLayer:
     def forward(self, logits, src, x, counts=None, out=None, taps=None, stream=None):
         if out is None:
             out = torch.empty((self.d.T, self.d.H), dtype=torch.bfloat16, device=self.device)
-        forward(self.d, logits, src, x, self.local_experts, self._w, counts, out, self.ws, taps, stream)
+        forward(self.d, logits, src, x, self.local_experts, self._w, counts, out, self.ws, taps, stream,
+                gating=self.gating)
         return out

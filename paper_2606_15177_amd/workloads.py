@@ -27,6 +27,7 @@ _TAG = {
     "w_gate": 6, "w_up": 7, "w_down": 8,
     "sh_gate": 9, "sh_up": 10, "sh_down": 11,
     "place_counts": 12, "place_bias": 13, "place_x0": 14, "place_m": 15,
+    "gate_bias": 16,
 }
 
 WEIGHT_STD = 0.02
@@ -51,12 +52,24 @@ class MoeConfig:
     hot_bias: float = 0.0
     src_layout: str = "uniform"   # uniform | blocks | interleaved
     local_layout: str = "all"     # all (identity) | choice (random subset)
+    # router gate function (moe_dims.flags: 0 softmax over the picks, 1 full
+    # softmax, 2 sigmoid) and its parameters
+    gate: int = 0
+    gate_bias_std: float = 0.0    # selection-only bias N(0, std) per expert (sigmoid gates)
+    routed_scale: float = 1.0
+    n_group: int = 0
+    topk_group: int = 0
 
     @property
     def dims(self) -> dict:
         return dict(T=self.T, H=self.H, E=self.E, k=self.k, I=self.I, S=self.S,
                     E_local=self.E_local, n_shared=self.n_shared,
                     I_shared=self.I_shared if self.n_shared else 0)
+
+    @property
+    def gated(self) -> bool:
+        """Whether the router differs from the default (softmax over the picks)."""
+        return bool(self.gate or self.gate_bias_std or self.routed_scale != 1.0 or self.n_group > 1)
 
     def replace(self, **kw) -> "MoeConfig":
         return dataclasses.replace(self, **kw)
@@ -83,6 +96,13 @@ CONFIGS: dict[str, MoeConfig] = {
         src_layout="blocks", local_layout="choice"),
 }
 CONFIG_ORDER = list(CONFIGS)
+
+# The DeepSeek-V3 share again with DeepSeek-V3's own router: sigmoid scores
+# with a selection-only bias, 8 groups of 32 experts of which 4 stay, routed
+# scale 2.5.  Not one of the five workloads above; a second routing family on
+# the same kernels.
+CONFIGS["ep_share_dsv3_v3router"] = CONFIGS["ep_share_dsv3"].replace(
+    name="ep_share_dsv3_v3router", gate=2, gate_bias_std=0.02, routed_scale=2.5, n_group=8, topk_group=4)
 
 
 def _rng(seed: int, tag: str, *extra: int) -> np.random.Generator:
@@ -221,10 +241,18 @@ def make_weights(cfg: MoeConfig, seed: int = 0, experts=None) -> dict:
     return out
 
 
+def make_gate_bias(cfg: MoeConfig, seed: int = 0) -> np.ndarray | None:
+    """The router's selection-only bias [E] fp32 (None when the router has none)."""
+    if not cfg.gate_bias_std:
+        return None
+    return (_rng(seed, "gate_bias").standard_normal(cfg.E) * cfg.gate_bias_std).astype(np.float32)
+
+
 def make_routing(cfg: MoeConfig, seed: int = 0) -> dict:
-    """The cheap part of a workload: src, logits and the local-expert list."""
+    """The cheap part of a workload: src, logits, the router's bias and the
+    local-expert list."""
     src = make_src(cfg, seed)
-    return dict(src=src, logits=make_logits(cfg, src, seed),
+    return dict(src=src, logits=make_logits(cfg, src, seed), gate_bias=make_gate_bias(cfg, seed),
                 local_experts=make_local_experts(cfg, seed))
 
 

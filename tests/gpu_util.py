@@ -79,3 +79,28 @@ def sample_tokens(T: int, n: int, seed: int = 0, extra=()) -> np.ndarray:
     rng = np.random.default_rng(seed)
     pick = set(rng.choice(T, size=min(n, T), replace=False).tolist()) | {0, T - 1} | set(extra)
     return np.array(sorted(pick), dtype=np.int32)
+
+
+def oracle_route_cfg(cfg, wl):
+    """The oracle's routing of a workload under its router's gate function."""
+    from oracle import oracle
+    if not cfg.gated:
+        return oracle.route(wl["logits"], cfg.k)
+    return oracle.route_gated(wl["logits"], cfg.k, cfg.gate, wl.get("gate_bias"), cfg.routed_scale,
+                              cfg.n_group, cfg.topk_group)
+
+
+def oracle_forward_cfg(cfg, wl, tokens):
+    from oracle import oracle
+    return oracle.forward_tokens(cfg.dims, tokens, wl["logits"], wl["x"], wl["local_experts"], wl,
+                                 gate=cfg.gate, bias=wl.get("gate_bias"), scale=cfg.routed_scale,
+                                 n_group=cfg.n_group, topk_group=cfg.topk_group)
+
+
+def gating_cfg(moe, cfg, wl, keep=None):
+    """(MoeGating or None, the device bias tensor it points to) for a workload."""
+    if not cfg.gated:
+        return None, None
+    b = wl.get("gate_bias")
+    bias = None if b is None else dev(b)
+    return moe.gating(bias, cfg.routed_scale, cfg.n_group, cfg.topk_group), bias

@@ -30,7 +30,7 @@ def test_exports_every_declared_function(moe):
 
 
 def test_abi_version_and_strerror(moe):
-    assert moe._lib.moe_abi_version() == 1
+    assert moe._lib.moe_abi_version() == 2
     for code in (0, -1, -2, -3, -4, -5, -6):
         assert moe.strerror(code) and moe.strerror(code) != "unknown status"
     assert moe.strerror(-99) == "unknown status"
@@ -62,7 +62,7 @@ def test_forward_workspace_size(moe):
     (dict(E_local=0), -2), (dict(E_local=9), -2), (dict(n_shared=-1), -2),
     (dict(n_shared=1, I_shared=0), -2), (dict(I=0), -2),
     (dict(H=12), -3), (dict(I=100), -3), (dict(n_shared=1, I_shared=36), -3),
-    (dict(E=1025, E_local=8), -3), (dict(E=64, k=33), -3), (dict(flags=1), -3),
+    (dict(E=1025, E_local=8), -3), (dict(E=64, k=33), -3), (dict(flags=3), -3), (dict(flags=-1), -3),
     (dict(T=2 ** 30, k=2), -3),
 ])
 def test_validate_rejects(moe, change, code):
@@ -78,8 +78,8 @@ def test_entry_points_reject_before_launch(moe):
     """Errors are decided on the host; nothing reaches the device."""
     lib = moe._lib
     d = moe.dims(T=4, H=64, E=8, k=2, I=64, S=2, E_local=4)
-    assert lib.moe_route(None, None, None, None, None) == moe.MOE_ERR_NULL
-    assert lib.moe_route(C.byref(d), None, None, None, None) == moe.MOE_ERR_NULL
+    assert lib.moe_route(None, None, None, None, None, None) == moe.MOE_ERR_NULL
+    assert lib.moe_route(C.byref(d), None, None, None, None, None) == moe.MOE_ERR_NULL
     assert lib.moe_route_stats(C.byref(d), None, None, None, None, None) == moe.MOE_ERR_NULL
     # no placement list while E_local < E
     assert lib.moe_permute(C.byref(d), 16, None, None, 16, 16, 16, None, None, 0, None) == moe.MOE_ERR_DIMS
@@ -98,12 +98,12 @@ def test_entry_points_reject_before_launch(moe):
     dsh = moe.dims(T=4, H=64, E=8, k=2, I=64, S=2, E_local=8, n_shared=1, I_shared=64)
     assert lib.moe_expert_ffn(C.byref(dsh), 16, 16, C.byref(w), None, 16, None, None, 0, None) == moe.MOE_ERR_NULL
     assert lib.moe_combine(C.byref(d8), None, 16, 16, None, 16, None) == moe.MOE_ERR_NULL
-    assert lib.moe_forward(C.byref(d8), 16, None, 16, None, C.byref(w), 16, 16, None, None, 0,
+    assert lib.moe_forward(C.byref(d8), None, 16, None, 16, None, C.byref(w), 16, 16, None, None, 0,
                            None) == moe.MOE_ERR_NULL       # counts without src
     ws_need = moe.workspace_bytes(d8, moe.ENTRY_FORWARD)
-    assert lib.moe_forward(C.byref(d8), 16, 16, 16, None, C.byref(w), 16, 16, None, 256, ws_need - 1,
+    assert lib.moe_forward(C.byref(d8), None, 16, 16, 16, None, C.byref(w), 16, 16, None, 256, ws_need - 1,
                            None) == moe.MOE_ERR_WORKSPACE
-    assert lib.moe_forward(C.byref(d8), 16, 16, 16, None, C.byref(w), 16, 16, None, 128, ws_need,
+    assert lib.moe_forward(C.byref(d8), None, 16, 16, 16, None, C.byref(w), 16, 16, None, 128, ws_need,
                            None) == moe.MOE_ERR_ALIGN      # workspace not 256-byte aligned
 
 
@@ -183,3 +183,24 @@ def test_window_alignment_and_empty(moe):
     wd0 = moe.MoeWindowDims(L=0, S=2, E=8, G=4, n_engines=4)
     assert lib.moe_window_stats(C.byref(wd0), None, None, None, None, None, None, None, None, None,
                                 None) == moe.MOE_OK
+
+
+@pytest.mark.parametrize("flags,g,code", [
+    (0, dict(bias=16), -2),                           # a bias needs sigmoid gates
+    (2, dict(bias=18), -6),                           # misaligned bias
+    (2, dict(n_group=3, topk_group=1), -2),           # 8 experts do not split into 3 groups
+    (2, dict(n_group=4, topk_group=0), -2),
+    (2, dict(n_group=4, topk_group=5), -2),
+    (2, dict(n_group=4, topk_group=1), -2),           # k=4 > 1 group of 2 experts
+    (2, dict(n_group=-1), -2),
+    (2, dict(n_group=128, topk_group=1), -3),
+    (1, dict(n_group=4, topk_group=2), -1),           # valid: fails later on the NULL logits
+    (2, dict(bias=16, n_group=2, topk_group=2, routed_scale=2.5), -1),
+])
+def test_gating_rejects_before_launch(moe, flags, g, code):
+    d = moe.dims(T=4, H=64, E=8, k=4, I=64, S=2, E_local=8, flags=flags)
+    n_group = g.get("n_group", 0)
+    if n_group == 128:
+        d = moe.dims(T=4, H=64, E=256, k=4, I=64, S=2, E_local=256, flags=flags)
+    gat = moe.MoeGating(g.get("bias"), g.get("routed_scale", 1.0), n_group, g.get("topk_group", 0))
+    assert moe._lib.moe_route(C.byref(d), C.byref(gat), None, None, None, None) == code

@@ -9,8 +9,8 @@ import torch
 
 from oracle import oracle
 from paper_2606_15177_amd import workloads as W
-from tests.gpu_util import (assert_gates_close, assert_layer_close, dev, dev_weights, host_bf16,
-                            sample_tokens, workload)
+from tests.gpu_util import (assert_gates_close, assert_layer_close, dev, dev_weights, gating_cfg, host_bf16,
+                            oracle_forward_cfg, oracle_route_cfg, sample_tokens, workload)
 
 pytestmark = pytest.mark.gpu
 
@@ -32,7 +32,8 @@ def _forward(moe, cfg, wl, counts=None, repeat=1):
                   inv_pos=torch.full((max(T * k, 1),), -9, dtype=torch.int32, device="cuda"))
     taps = moe.make_taps(**taps_t)
     loc = None if wl["local_experts"] is None else dev(wl["local_experts"])
-    layer = moe.MoeLayer(d, dev_weights(wl), loc)
+    gating, gate_bias = gating_cfg(moe, cfg, wl)
+    layer = moe.MoeLayer(d, dev_weights(wl), loc, gating=gating)
     if counts is None:
         counts = torch.zeros((cfg.S, cfg.E), dtype=torch.int64, device="cuda")
     logits, src, x = dev(wl["logits"]), dev(wl["src"]), dev(wl["x"])
@@ -50,7 +51,7 @@ def _forward(moe, cfg, wl, counts=None, repeat=1):
 
 def _check_routing(cfg, wl, res, calls=1):
     T, k = cfg.T, cfg.k
-    ridx, rw = oracle.route(wl["logits"], k)
+    ridx, rw = oracle_route_cfg(cfg, wl)
     np.testing.assert_array_equal(res["topk_idx"][:T], ridx)
     assert_gates_close(res["topk_w"][:T], rw, cfg.name)
     rc, rl = oracle.route_stats(wl["src"], ridx, cfg.S, cfg.E)
@@ -145,3 +146,34 @@ def test_forward_full_size(moe, name):
     ref = oracle.forward_tokens(cfg.dims, toks, wl["logits"], wl["x"], wl["local_experts"], wl)
     e = assert_layer_close(res["outs"][0][toks], ref, name)
     print(f"{name}: rel {e['rel']:.2e} mae {e['mae']:.2e} rel_mae {e['rel_mae']:.2e}")
+
+
+@pytest.mark.parametrize("variant", [
+    dict(gate=1),
+    dict(gate=1, n_group=4, topk_group=2, routed_scale=2.0),
+    dict(gate=2, gate_bias_std=0.05, routed_scale=2.5, n_group=4, topk_group=2),
+    dict(gate=2, gate_bias_std=0.05, E=64, k=6, E_local=20, local_layout="choice", n_group=8, topk_group=3,
+         n_shared=1, I_shared=128, T=513),
+])
+def test_forward_gated_routers(moe, variant):
+    """The layer under each gating variant: routing bit-exact, output within
+    the layer tolerance against the oracle's layer with the same router."""
+    cfg = W.CONFIGS["tiny"].replace(**{**dict(name="gated", E=16, k=4, E_local=16, T=300), **variant})
+    wl = W.make_workload(cfg, seed=7)
+    res = _forward(moe, cfg, wl)
+    _check_routing(cfg, wl, res)
+    ref = oracle_forward_cfg(cfg, wl, np.arange(cfg.T))
+    assert_layer_close(res["outs"][0], ref, str(variant))
+
+
+@pytest.mark.slow
+def test_forward_v3_router_full_size_sampled(moe):
+    """The DeepSeek-V3 share with DeepSeek-V3's router at full size: routing
+    and dispatch bit-exact, sampled tokens of the output against the oracle."""
+    cfg = W.CONFIGS["ep_share_dsv3_v3router"]
+    wl = workload(cfg.name)
+    res = _forward(moe, cfg, wl)
+    _check_routing(cfg, wl, res)
+    toks = sample_tokens(cfg.T, 12, seed=1)
+    ref = oracle_forward_cfg(cfg, wl, toks)
+    assert_layer_close(res["outs"][0][toks], ref, cfg.name)

@@ -121,3 +121,59 @@ def test_stats_global_atomic_path_and_bad_ids(moe):
         c, load = _stats(moe, src, idx, S, E)
         np.testing.assert_array_equal(c.cpu().numpy(), rc)
         np.testing.assert_array_equal(load, rl)
+
+
+# ------------------------------------------------------ gating variants ---
+
+def _route_gated(moe, logits, k, gate, bias=None, scale=1.0, n_group=0, topk_group=0):
+    T, E = logits.shape
+    d = moe.dims(T=T, H=8, E=E, k=k, I=8, S=1, E_local=E, flags=gate)
+    b = None if bias is None else dev(bias)
+    g = moe.gating(b, scale, n_group, topk_group)
+    idx = torch.full((T, k), -7, dtype=torch.int32, device="cuda")
+    w = torch.full((T, k), -7.0, dtype=torch.float32, device="cuda")
+    moe.route(d, dev(logits), idx, w, gating=g)
+    torch.cuda.synchronize()
+    return idx.cpu().numpy(), w.cpu().numpy()
+
+
+GATED_CASES = [  # (E, k, gate, with bias, scale, n_group, topk_group)
+    (8, 2, 1, False, 1.0, 0, 0), (64, 6, 1, False, 1.0, 0, 0), (256, 8, 1, False, 16.0, 8, 3),
+    (8, 2, 2, True, 2.5, 4, 2), (64, 6, 2, True, 1.0, 8, 3), (256, 8, 2, True, 2.5, 8, 4),
+    (256, 8, 2, False, 1.0, 0, 0), (160, 6, 2, True, 2.5, 5, 2), (1024, 16, 2, True, 1.0, 64, 8),
+    (12, 3, 2, True, 1.0, 12, 3), (96, 4, 0, False, 3.0, 6, 2), (33, 5, 2, True, 1.0, 0, 0),
+]
+
+
+@pytest.mark.parametrize("E,k,gate,with_bias,scale,n_group,topk_group", GATED_CASES)
+def test_route_gated_variants(moe, E, k, gate, with_bias, scale, n_group, topk_group):
+    rng = np.random.default_rng(E * 31 + k * 7 + gate)
+    T = 700
+    logits = rng.standard_normal((T, E)).astype(np.float32) * 2
+    logits[:100] = np.round(logits[:100])                       # ties
+    logits[100:150, rng.integers(0, E, 3)] = np.nan
+    logits[150:200, rng.integers(0, E, 3)] = -np.inf
+    logits[200:220, rng.integers(0, E, 2)] = np.inf
+    bias = (rng.standard_normal(E) * 0.05).astype(np.float32) if with_bias else None
+    if with_bias:
+        bias[:: max(1, E // 7)] = np.round(bias[:: max(1, E // 7)] * 8) / 8
+    idx, w = _route_gated(moe, logits, k, gate, bias, scale, n_group, topk_group)
+    ridx, rw = oracle.route_gated(logits, k, gate, bias, scale, n_group, topk_group)
+    np.testing.assert_array_equal(idx, ridx)
+    finite = np.isfinite(rw)
+    np.testing.assert_array_equal(np.isfinite(w), finite)
+    np.testing.assert_allclose(w[finite], rw[finite], rtol=0, atol=1e-6 * max(1.0, scale))
+
+
+def test_route_v3_router_full_size(moe):
+    """The DeepSeek-V3 router on the full 16384-token, 256-expert workload."""
+    cfg = W.CONFIGS["ep_share_dsv3_v3router"]
+    r = W.make_routing(cfg, seed=0)
+    idx, w = _route_gated(moe, r["logits"], cfg.k, cfg.gate, r["gate_bias"], cfg.routed_scale, cfg.n_group,
+                          cfg.topk_group)
+    ridx, rw = oracle.route_gated(r["logits"], cfg.k, cfg.gate, r["gate_bias"], cfg.routed_scale, cfg.n_group,
+                                  cfg.topk_group)
+    np.testing.assert_array_equal(idx, ridx)
+    np.testing.assert_allclose(w, rw, rtol=0, atol=1e-6 * cfg.routed_scale)
+    # only 4 of the 8 groups per token
+    assert (np.array([len(set(row // 32)) for row in idx]) <= 4).all()
