@@ -31,6 +31,7 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kLdsBinsMax = 16384;  // S*E bins kept in LDS (64 KB)
+constexpr int kStatsPairs = 2048;   // (token, expert) pairs per block of the counting kernel
 
 __device__ __forceinline__ uint32_t order_key(float f) {
   if (f != f) return 0u;            // NaN: below every number
@@ -89,18 +90,51 @@ __device__ __forceinline__ float sigmoid_score(float l) {
   return static_cast<float>(1.0 / (1.0 + exp(-static_cast<double>(l))));
 }
 
-template <int G>
-__device__ __forceinline__ uint64_t group_max64(uint64_t v) {
-#pragma unroll
-  for (int off = G / 2; off > 0; off >>= 1)
-    v = umax64(v, __shfl_xor(static_cast<unsigned long long>(v), off, G));
-  return v;
+// Butterfly levels within a 16-lane row by DPP (quad swaps, then the half-row
+// and row mirrors), across rows by ds_bpermute.  Max and sum are symmetric,
+// so after the levels every lane of a G-lane group holds the group's result.
+template <int CTRL>
+__device__ __forceinline__ int dpp_i32(int v) {
+  return __builtin_amdgcn_update_dpp(v, v, CTRL, 0xf, 0xf, false);
+}
+constexpr int kDppSwap1 = 0xB1;       // quad_perm [1, 0, 3, 2]
+constexpr int kDppSwap2 = 0x4E;       // quad_perm [2, 3, 0, 1]
+constexpr int kDppHalfMirror = 0x141;  // lane i <-> 7 - i within 8 lanes
+constexpr int kDppMirror = 0x140;      // lane i <-> 15 - i within 16 lanes
+
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t v) {
+  const int lo = dpp_i32<CTRL>(static_cast<int>(static_cast<uint32_t>(v)));
+  const int hi = dpp_i32<CTRL>(static_cast<int>(static_cast<uint32_t>(v >> 32)));
+  return (static_cast<uint64_t>(static_cast<uint32_t>(hi)) << 32) | static_cast<uint32_t>(lo);
 }
 
 template <int G>
+__device__ __forceinline__ uint64_t group_max64(uint64_t v) {
+  if constexpr (G > 1) v = umax64(v, dpp_u64<kDppSwap1>(v));
+  if constexpr (G > 2) v = umax64(v, dpp_u64<kDppSwap2>(v));
+  if constexpr (G > 4) v = umax64(v, dpp_u64<kDppHalfMirror>(v));
+  if constexpr (G > 8) v = umax64(v, dpp_u64<kDppMirror>(v));
+  if constexpr (G > 16) v = umax64(v, __shfl_xor(static_cast<unsigned long long>(v), 16));
+  if constexpr (G > 32) v = umax64(v, __shfl_xor(static_cast<unsigned long long>(v), 32));
+  return v;
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __int_as_float(dpp_i32<CTRL>(__float_as_int(v)));
+}
+
+// Each level adds the same two partial sums on both lanes of a pair, so every
+// lane of the group ends with the same bits.
+template <int G>
 __device__ __forceinline__ float group_sum(float v) {
-#pragma unroll
-  for (int off = G / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, G);
+  if constexpr (G > 1) v += dpp_f32<kDppSwap1>(v);
+  if constexpr (G > 2) v += dpp_f32<kDppSwap2>(v);
+  if constexpr (G > 4) v += dpp_f32<kDppHalfMirror>(v);
+  if constexpr (G > 8) v += dpp_f32<kDppMirror>(v);
+  if constexpr (G > 16) v += __shfl_xor(v, 16);
+  if constexpr (G > 32) v += __shfl_xor(v, 32);
   return v;
 }
 
@@ -215,8 +249,7 @@ __global__ __launch_bounds__(kBlock) void route_kernel(RouteKernelArgs a) {
 #pragma unroll
       for (int v = 0; v < V; ++v)
         if (lg[v] == lg[v]) mk = max(mk, order_key(lg[v]));
-#pragma unroll
-      for (int off = G / 2; off > 0; off >>= 1) mk = max(mk, static_cast<uint32_t>(__shfl_xor(static_cast<int>(mk), off, G)));
+      mk = static_cast<uint32_t>(group_max64<G>(mk) & 0xffffffffu);
       const float M = mk ? key_value(mk) : __builtin_nanf("");
       float part = 0.0f;
 #pragma unroll
@@ -276,9 +309,9 @@ template <int G, int V, bool EXT>
 hipError_t launch_route_gv(const RouteKernelArgs& in, hipStream_t st) {
   constexpr int kGroups = kBlock / G;
   RouteKernelArgs a = in;
-  // 4 tokens per group and block keeps the histogram flush amortised while
-  // leaving enough blocks to fill the chip at the prefill sizes.
-  a.tokens_per_block = kGroups * 4;
+  // One token per group and block: the selection is a chain of dependent
+  // lane reductions, so many resident blocks hide its latency.
+  a.tokens_per_block = kGroups;
   const int blocks = ceil_div(a.T, a.tokens_per_block);
   a.lds_bins = (a.counts && a.S * a.E <= kLdsBinsMax) ? a.S * a.E : 0;
   const size_t lds = a.lds_bins * sizeof(int) + ((EXT && a.n_group > 1) ? sizeof(float) * kGroups * a.E : 0);
@@ -329,13 +362,14 @@ hipError_t launch_route(int T, int E, int k, const float* logits, int32_t* topk_
   a.expert_load = expert_load;
   a.scale = 1.0f;
   const bool ext = gating && (gating->gate != 0 || gating->bias || gating->n_group > 1 || gating->scale != 1.0f);
-  if (!ext) return launch_route_ext<false>(a, st);
-  a.gate = gating->gate;
-  a.bias = gating->bias;
-  a.scale = gating->scale;
-  a.n_group = gating->n_group;
-  a.topk_group = gating->topk_group;
-  return launch_route_ext<true>(a, st);
+  if (ext) {
+    a.gate = gating->gate;
+    a.bias = gating->bias;
+    a.scale = gating->scale;
+    a.n_group = gating->n_group;
+    a.topk_group = gating->topk_group;
+  }
+  return ext ? launch_route_ext<true>(a, st) : launch_route_ext<false>(a, st);
 }
 
 hipError_t launch_route_stats(int T, int k, int S, int E, const int32_t* src,
@@ -343,7 +377,7 @@ hipError_t launch_route_stats(int T, int k, int S, int E, const int32_t* src,
                               hipStream_t st) {
   const int n_pairs = T * k;
   if (n_pairs == 0) return hipSuccess;
-  const int pairs_per_block = 2048;
+  const int pairs_per_block = kStatsPairs;
   const int blocks = ceil_div(n_pairs, pairs_per_block);
   const int bins = (S * E <= kLdsBinsMax) ? S * E : 0;
   hipLaunchKernelGGL(stats_kernel, dim3(blocks), dim3(kBlock), bins * sizeof(int), st, n_pairs, k,
