@@ -13,6 +13,7 @@ namespace moe {
 namespace {
 
 constexpr int kMaxK = 32;
+constexpr int kLoadsInFlight = 8;  // row loads a lane issues before it accumulates
 
 __global__ __launch_bounds__(256) void combine_kernel(int T, int k, int H,
                                                       const uint16_t* __restrict__ y_perm,
@@ -42,15 +43,26 @@ __global__ __launch_bounds__(256) void combine_kernel(int T, int k, int H,
       const int v = v0 + lane;
       const bool active = v < vpr;
       float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-      for (int j = 0; j < k; ++j) {
-        const int r = __shfl(pos, j);
-        const float wj = __shfl(w, j);
-        if (r < 0 || !active) continue;
-        const u32x4 q = load16(y_perm + static_cast<size_t>(r) * H + v * 8);
+      // eight rows' loads are issued before the first of them is consumed;
+      // the sum still runs in j order, and a pair without a local row adds
+      // nothing (not even 0 * its gate)
+      for (int j0 = 0; j0 < k; j0 += kLoadsInFlight) {
+        int r[kLoadsInFlight];
+        u32x4 q[kLoadsInFlight];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc[2 * e] = fmaf(wj, __uint_as_float(q[e] << 16), acc[2 * e]);
-          acc[2 * e + 1] = fmaf(wj, __uint_as_float(q[e] & 0xffff0000u), acc[2 * e + 1]);
+        for (int jj = 0; jj < kLoadsInFlight; ++jj) {
+          r[jj] = j0 + jj < k ? __builtin_amdgcn_readlane(pos, j0 + jj) : -1;   // wave-uniform
+          q[jj] = (r[jj] >= 0 && active) ? load16(y_perm + static_cast<size_t>(r[jj]) * H + v * 8) : u32x4{0, 0, 0, 0};
+        }
+#pragma unroll
+        for (int jj = 0; jj < kLoadsInFlight; ++jj) {
+          const float wj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), j0 + jj < k ? j0 + jj : 0));
+          if (r[jj] < 0) continue;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            acc[2 * e] = fmaf(wj, __uint_as_float(q[jj][e] << 16), acc[2 * e]);
+            acc[2 * e + 1] = fmaf(wj, __uint_as_float(q[jj][e] & 0xffff0000u), acc[2 * e + 1]);
+          }
         }
       }
       if (!active) continue;
