@@ -46,6 +46,8 @@ def parse_args(argv=None):
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="budget of the CPU-oracle baseline sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--gpu-metrics", action="store_true",
+                   help="sample the shader clock and socket power with amd-smi during the run")
     p.add_argument("--fenced-events", action="store_true",
                    help="time with default (system-fenced) HIP events instead of timing-only ones")
     p.add_argument("--calib-copy-mib", type=int, default=0,
@@ -146,52 +148,33 @@ def measured_traffic(stage: str, workload: str):
     return float(m_b.group(1))
 
 
-def sample_gpu_metrics(busy_step, max_s: float = 20.0) -> dict:
-    """Clock and power of GPU 0 sampled by amd-smi while busy_step() keeps the
-    GPU busy (best effort: an empty dict when the tool is missing or fails)."""
-    import subprocess
-    import threading
+class GpuMetricsWatch:
+    """amd-smi clock and power samples of GPU 0, once a second, for the whole
+    run.  The watcher is started as a child process before this process
+    touches the GPU (a process that has initialised the GPU must not start
+    programs), so it is opt-in (--gpu-metrics) and refused under a profiler,
+    whose preloaded library initialises the GPU before the program starts."""
 
-    import torch
-    out = {}
+    def __init__(self):
+        import subprocess
+        if any("rocprof" in v for k, v in os.environ.items() if k in ("LD_PRELOAD", "HSA_TOOLS_LIB")):
+            raise SystemExit("--gpu-metrics cannot run under a profiler")
+        self.proc = subprocess.Popen(["amd-smi", "metric", "-c", "-p", "--json", "-g", "0", "-w", "1"],
+                                     stdout=subprocess.PIPE, stderr=subprocess.DEVNULL, text=True)
 
-    def sample():
+    def stop(self) -> dict:
+        self.proc.terminate()
         try:
-            r = subprocess.run(["amd-smi", "metric", "-c", "-p", "--json", "-g", "0"], capture_output=True,
-                               text=True, timeout=max_s)
-            out["raw"] = r.stdout
-        except Exception as e:  # noqa: BLE001 - a missing tool only loses the sample
-            out["error"] = str(e)
-
-    th = threading.Thread(target=sample)
-    th.start()
-    t0 = time.perf_counter()
-    while th.is_alive() and time.perf_counter() - t0 < max_s + 5:
-        for _ in range(20):
-            busy_step()
-        torch.cuda.synchronize()
-    th.join(timeout=1.0)
-    res = {}
-    try:
-        data = json.loads(out.get("raw", ""))
-        gpu = data[0] if isinstance(data, list) else data
-        if isinstance(gpu, dict) and "gpu_data" in gpu:
-            gpu = gpu["gpu_data"][0]
-
-        def val(d, *keys):
-            for k in keys:
-                if not isinstance(d, dict) or k not in d:
-                    return None
-                d = d[k]
-            return d.get("value") if isinstance(d, dict) else d
-
-        res = {"sclk_mhz": val(gpu, "clock", "gfx_0", "clk"), "mclk_mhz": val(gpu, "clock", "mem_0", "clk"),
-               "socket_power_w": val(gpu, "power", "socket_power")}
-    except Exception:  # noqa: BLE001
-        res = {}
-    if not any(v is not None for v in res.values()):
-        res = {"unparsed": (out.get("raw") or out.get("error") or "")[:400]}
-    return res
+            text, _ = self.proc.communicate(timeout=10)
+        except Exception:  # noqa: BLE001 - a watcher that hangs only loses its samples
+            self.proc.kill()
+            return {}
+        sclk = [int(m) for m in re.findall(r'"gfx_0":\s*\{\s*"clk":\s*\{\s*"value":\s*(\d+)', text)]
+        power = [int(m) for m in re.findall(r'"socket_power":\s*\{\s*"value":\s*(\d+)', text)]
+        if not sclk:
+            return {}
+        return {"samples": len(sclk), "sclk_mhz_max": max(sclk), "sclk_mhz_min": min(sclk),
+                "socket_power_w_max": max(power) if power else None}
 
 
 def cpu_baseline(cfg, wl, budget_s: float) -> dict:
@@ -323,7 +306,11 @@ def main(argv=None) -> int:
         return 2
     if args.config.startswith("place_"):
         return bench_place(args)
+    return bench_layer(args, GpuMetricsWatch() if args.gpu_metrics else None)  # watcher before any GPU use
 
+
+def bench_layer(args, watch) -> int:
+    """Throughput of moe_forward on a layer workload (one JSON line)."""
     import numpy as np
     import torch
 
@@ -450,7 +437,6 @@ def main(argv=None) -> int:
     ffn_bytes = work["ffn_up"]["bytes"] + work["ffn_down"]["bytes"]
     ffn_frac_hbm = ffn_bytes / (ffn_ms * 1e-3) / (HBM_PEAK_GBS * 1e9) if ffn_ms > 0 else 0.0
 
-    metrics = sample_gpu_metrics(lambda: layer.forward(logits, src, x, counts, out, plain_taps))
 
     if args.calib_copy_mib:
         n = args.calib_copy_mib * (1 << 20)
@@ -494,7 +480,7 @@ def main(argv=None) -> int:
                  "note": "1 GiB written before each step; GPU time of the step"},
         "stats_collection": {"route_ms_with_counts": round(stage_ms["route"], 4),
                              "route_ms_without_counts": round(route_no_stats, 4)},
-        "gpu_metrics": metrics,
+        **({"gpu_metrics": watch.stop()} if watch else {}),
         "rows_local": R,
         "active_experts": active,
         "device": torch.cuda.get_device_name(0),
