@@ -23,10 +23,14 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
   return __builtin_bit_cast(uint16_t, h);
 }
 
-// Two fp32 -> packed bf16 pair (low half = a).
+// Two fp32 -> packed bf16 pair (low half = a), round-to-nearest-even: one
+// v_cvt_pk_bf16_f32 for both values.
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-  return static_cast<uint32_t>(f32_to_bf16(a)) | (static_cast<uint32_t>(f32_to_bf16(b)) << 16);
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){a, b}, bf16x2));
 }
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float a, float b) { return pack_bf16x2(a, b); }
 
 __device__ __forceinline__ u32x4 load16(const void* p) {
   return *reinterpret_cast<const u32x4*>(p);
@@ -40,7 +44,10 @@ __device__ __forceinline__ void store16(void* p, u32x4 v) {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-__device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }
+// silu(z) = z * sigmoid(z), with the hardware reciprocal (about 1 ulp) in
+// place of an IEEE division: a correctly rounded quotient costs ten
+// instructions per value in the GEMM epilogues.
+__device__ __forceinline__ float silu(float z) { return z * __builtin_amdgcn_rcpf(1.0f + __expf(-z)); }
 
 __device__ __forceinline__ int lane_id() { return static_cast<int>(threadIdx.x) & (kWave - 1); }
 

@@ -1,5 +1,5 @@
 // Expert FFN for prefill-sized batches: a persistent bf16 MFMA grouped GEMM
-// with direct-to-LDS loads and two ping-pong wave groups.
+// with direct-to-LDS loads, one wave per SIMD.
 //
 // Tiles.  An output tile is 256 token rows x 256 weight rows of one group
 // (expert).  For the gate/up GEMM the 256 weight rows are 128 gate rows and
@@ -13,52 +13,63 @@
 // the weights are fetched from HBM once.  Group sizes never leave the
 // device.
 //
+// Waves.  Four waves, one per SIMD; wave (wm, wn) owns token rows
+// 128*wm .. +127 and weight rows 128*wn .. +127 of the tile: 4 x 4
+// v_mfma_f32_32x32x16_bf16 tiles (weights as the A operand, tokens as B),
+// 256 fp32 accumulators held in AGPRs.
+//
 // Stages.  K advances in stages of 32.  A stage holds X[256 x 32] and
 // W[256 x 32] in LDS (64-byte rows, 32 KB) and is filled by
 // buffer_load_dwordx4 ... lds, which writes 64 lanes x 16 bytes to
-// consecutive LDS addresses without passing through registers.  Four stages
-// form a ring: the loads of stage j+3 are issued while stage j is consumed,
-// so a load has about three stage times to arrive, and the stage sequence
-// runs on across tile boundaries (the next tile's first stages are in flight
-// during a tile's last ones).  Chunk c (16 bytes) of LDS row r sits at slot
-// c ^ ((r >> 2) & 3): every lane of a load fetches the global chunk that
-// belongs at its fixed LDS slot, and the 16 rows that 16 lanes of an MFMA
-// fragment read land in 16 distinct bank groups.  Rows past a group's end,
-// columns past N and the K tail get byte offsets >= 2^31, past the buffer
-// descriptor's range: they read as zeros and cost no memory traffic.
+// consecutive LDS addresses without passing through registers; each wave
+// fills 64 rows of each part.  Four stages form a ring.  Chunk c (16 bytes)
+// of LDS row r sits at slot c ^ ((r >> 2) & 3): every lane of a load fetches
+// the global chunk that belongs at its fixed LDS slot, and the 16 rows that
+// 16 lanes of an MFMA fragment read land in 16 distinct bank groups.  Rows
+// past a group's end, columns past N and the K tail get byte offsets
+// >= 2^31, past the buffer descriptor's range: they read as zeros and cost
+// no memory traffic.
 //
-// Ping-pong.  The 8 waves form two groups of four, one wave of each group
-// per SIMD.  Group 0 computes token rows 0..127 of the tile and group 1 rows
-// 128..255; a wave owns 64 token rows x 128 weight rows (2 x 4 MFMA tiles of
-// v_mfma_f32_32x32x16_bf16, weights as the A operand, tokens as B).  The two
-// groups alternate, one phase apart, between a memory phase (issue loads,
-// read the stage's fragments from LDS into registers) and a compute phase
-// (16 MFMAs on registers only), with a workgroup barrier between phases: on
-// every SIMD one wave issues MFMAs while the other one feeds LDS.
+// Pipeline.  One workgroup barrier per stage, placed before its last K-step
+// after each wave has waited for its own loads of the next stage and for its
+// LDS reads: past it the next stage's data are in LDS and the stage's own
+// buffer is free.  The loads of stage j + 4 go into that buffer, spread one
+// per four MFMAs over the last K-step of stage j and the first of stage
+// j + 1: a burst of loads stalls the issuing wave (one wave per SIMD, in
+// order) while the address unit drains, and the MFMA pipe with it.  A load
+// has about three stage times to land; the stage sequence runs on across
+// tile boundaries.
 //
-// Waits.  Each wave issues the loads of stage j+3 for its part in its memory
-// phase of stage j and waits for its own loads of stage j+1 (s_waitcnt vmcnt
-// with the two younger stages' 8 loads still in flight) before the barrier
-// that precedes the first read of stage j+1; it waits for its LDS reads
-// (lgkmcnt(0)) before every barrier, so a buffer is refilled only after both
-// groups have read it.
+// Epilogue.  A lane holds row r, columns 8*v + 4*h + 0..3 (v < 4, h = lane
+// half) of each 32 x 32 accumulator tile.  Values are converted in bf16
+// pairs and a swap between the lane halves (v_permlane32_swap) gives every
+// lane 8 consecutive columns, written as one 16-byte store.
 #include "ffn_impl.h"
 
 namespace moe {
 namespace {
 
-constexpr int kBM = 256;                          // token rows per tile
-constexpr int kBN = 256;                          // weight rows per tile
-constexpr int kBK = 32;                           // K per stage
-constexpr int kStages = 4;                        // LDS ring depth
-constexpr int kThreads = 8 * kWave;
-constexpr int kRowBytes = kBK * 2;                // 64
-constexpr int kPartBytes = kBM * kRowBytes;       // one operand of a stage: 16 KB
-constexpr int kStageBytes = 2 * kPartBytes;       // X part, then W part
-constexpr int kLdsBytes = kStages * kStageBytes;  // 128 KB
-constexpr int kLoadsPerStage = 4;                 // per wave: 4 loads of 1 KB (group 0: X, group 1: W)
+constexpr int kBM = 256;                // token rows per tile
+constexpr int kBN = 256;                // weight rows per tile
+constexpr int kThreads = 4 * kWave;     // four waves, one per SIMD
 constexpr int kMaxGroups = 1024;
-static_assert(kBM == kBN && kBM * kRowBytes == 16 * 1024 * 1, "a stage part is 16 loads of 1 KB");
+
+// One K stage and the ring of them.
+struct Stage {
+  static constexpr int BK = 32;                   // K per stage
+  static constexpr int CPR = BK * 2 / 16;         // 16-byte chunks per LDS row
+  static constexpr int RPI = kWave / CPR;         // rows per load instruction
+  static constexpr int SWZ = 16 / CPR;            // rows sharing one swizzle key
+  static constexpr int ROW = BK * 2;              // bytes per LDS row
+  static constexpr int PART = kBM * ROW;          // one operand of a stage: 16 KB
+  static constexpr int STAGE = 2 * PART;          // X part, then W part
+  static constexpr int NS = 4;                    // ring depth
+  static constexpr int LDS = NS * STAGE;          // 128 KB
+  static constexpr int LPP = 64 / RPI;            // loads per part per wave
+  static constexpr int LPS = 2 * LPP;             // loads per stage per wave
+  static constexpr int KSTEPS = BK / 16;          // MFMA K-steps per stage
+};
+static_assert(kBM == kBN && Stage::RPI * Stage::ROW == 1024, "a load fills 1 KB of LDS rows");
 
 // s_waitcnt immediates (gfx9 layout: vmcnt [3:0] and [15:14], expcnt [6:4],
 // lgkmcnt [11:8]); a field at its maximum does not wait.
@@ -68,7 +79,7 @@ constexpr int kWaitAll = 0;
 
 // Workgroup barrier that also fences the compiler: no instruction is moved
 // across it, and memory accesses stay on their side (the hardware waits are
-// the explicit s_waitcnt above).
+// the explicit s_waitcnt).
 __device__ __forceinline__ void phase_barrier() {
   __builtin_amdgcn_sched_barrier(0);
   asm volatile("s_barrier" ::: "memory");
@@ -80,21 +91,30 @@ __device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t rs, unsigned c
   __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)lds, 16, voff, 0, 0, 0);
 }
 
+// The lane id, recomputed behind a volatile asm: values derived from it are
+// not hoisted out of loops by the compiler and hold no register across them.
+__device__ __forceinline__ int opaque_lane_id() {
+  int ln;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
+  return ln;
+}
+
 template <bool GATED>
-__global__ __launch_bounds__(kThreads) void tiled_kernel(GemmArgs a) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) void tiled_kernel(GemmArgs a) {
+  using C = Stage;
   constexpr int OUT_COLS = GATED ? kBN / 2 : kBN;
   constexpr uint32_t kInvalid = 0x80000000u;
   constexpr int kRecords = 0x7fffffff;
   constexpr int kRsrcWord3 = 0x00020000;
 
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  __shared__ int mt_prefix[kMaxGroups + 1];  // first m-tile of each group
-  __shared__ int row_off[kMaxGroups + 1];    // the group offsets, read once
+  __shared__ int mt_prefix[kMaxGroups + 1];
+  __shared__ int row_off[kMaxGroups + 1];
 
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
-  const int grp = wave >> 2, q = wave & 3;
+  const int wm = wave & 1, wn = wave >> 1;
   const int lrow = lane & 31, lhalf = lane >> 5;
   const int n_tiles_n = ceil_div(a.N, OUT_COLS);
 
@@ -128,23 +148,18 @@ __global__ __launch_bounds__(kThreads) void tiled_kernel(GemmArgs a) {
     total_mt = mt_prefix[a.groups];
   }
   const int total_tiles = total_mt * n_tiles_n;
-
-  // XCD-aware renumbering (gridDim.x is a multiple of 8)
   const int per_xcd = gridDim.x / 8;
   const int first = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
   if (first >= total_tiles) return;
-  const int nkb = ceil_div(a.K, kBK);
+  const int nkb = ceil_div(a.K, C::BK);
   const int n_stages = ceil_div(total_tiles - first, gridDim.x) * nkb;
 
   struct TileInfo {
     int g, row_base, m, m0, nt;
   };
-  // Tile order: group, then n-tile, then m-tile (fastest).  The m-tiles of a
-  // group that share one weight tile are neighbours, so they run at the same
-  // time on one XCD and the weights cross the fabric once.
   auto tile_info = [&](int t) {
     TileInfo ti;
-    int mg = total_mt, base = 0;  // m-tiles of the group, first tile id of the group
+    int mg = total_mt, base = 0;
     ti.g = 0;
     ti.row_base = 0;
     ti.m = a.static_rows;
@@ -154,8 +169,6 @@ __global__ __launch_bounds__(kThreads) void tiled_kernel(GemmArgs a) {
         const int mid = (lo + hi + 1) >> 1;
         if (mt_prefix[mid] * n_tiles_n <= t) lo = mid; else hi = mid - 1;
       }
-      // from LDS: a global load here would make the compiler wait for every
-      // stage load in flight (they share the vector memory counter)
       ti.g = lo;
       ti.row_base = row_off[lo];
       ti.m = row_off[lo + 1] - ti.row_base;
@@ -173,80 +186,94 @@ __global__ __launch_bounds__(kThreads) void tiled_kernel(GemmArgs a) {
     return ti;
   };
 
-  // ---- load side: runs three stages ahead of the compute side ----
-  // Group 0 fills the X part of every stage and group 1 the W part, each in
-  // its own memory phase, so no wave issues loads between its MFMAs.  Wave q
-  // of a group fills the 16-row blocks 4q..4q+3 of its part.  A lane's LDS
-  // slot is lane & 3 of row lane >> 2 of a block, so the global chunk it
-  // fetches, (lane & 3) ^ ((row >> 2) & 3), depends on the lane only.
-  const int chunk = (lane & 3) ^ ((lane >> 4) & 3);
-  __amdgpu_buffer_rsrc_t rs_ld;  // X (group 0) or W (group 1) of the tile being loaded
-  u32x4 ld_off;                  // byte offset of each load's row, or >= 2^31
+  // ---- load side: wave w fills rows 64w..64w+63 of both parts ----
+  // Load i writes rows 64w + RPI*i + lane/CPR, slot lane%CPR; the global
+  // chunk it fetches is slot ^ ((row / SWZ) % CPR).
+  const int lslot = lane % C::CPR;
+  __amdgpu_buffer_rsrc_t rs_x, rs_w0, rs_w1;
+  uint32_t xoff[C::LPP], woff[C::LPP];
   int ld_tile = first, ld_kb = 0;
-  auto ld_setup = [&](int t) {
-    if (t >= total_tiles) {  // past this workgroup's last tile: empty loads keep the count regular
-      ld_off = u32x4{kInvalid, kInvalid, kInvalid, kInvalid};
-      return;
-    }
+  auto ld_chunk_l = [&](int i, int ln) {
+    const int r = 64 * wave + C::RPI * i + ln / C::CPR;
+    return (ln % C::CPR) ^ ((r / C::SWZ) % C::CPR);
+  };
+  auto ld_chunk = [&](int i) { return ld_chunk_l(i, lane); };
+  auto ld_setup = [&](int t_in) {
+    // past this workgroup's last tile: the same loads with every offset
+    // marked invalid keep the load count regular (branch-free, so the
+    // offsets stay in registers)
+    const bool live = t_in < total_tiles;
+    const uint32_t dead = live ? 0u : kInvalid;
+    const int t = live ? t_in : total_tiles - 1;
     const TileInfo ti = tile_info(t);
-    if (grp == 0) {
-      // token rows: consecutive rows of x, or x rows named by x_rows (the
-      // dispatch gather done by the loads themselves)
-      const uint16_t* xb = a.x_rows ? a.x : a.x + static_cast<size_t>(ti.row_base + ti.m0) * a.K;
-      rs_ld = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(xb), 0, kRecords, kRsrcWord3);
-      // the four row indices are loaded together (rows past the group read
-      // the group's first index and are masked), so one wait covers them
-      int xr[4];
+    // opaque lane id: the per-lane row terms are recomputed here rather
+    // than hoisted out of the K loop
+    int ln = opaque_lane_id();
+    const uint16_t* xb = a.x_rows ? a.x : a.x + static_cast<size_t>(ti.row_base + ti.m0) * a.K;
+    rs_x = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(xb), 0, kRecords, kRsrcWord3);
+    int xr[C::LPP];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = 16 * (4 * q + i) + (lane >> 2);  // token row within the tile
-        xr[i] = r;
-        if (a.x_rows) xr[i] = a.x_rows[ti.row_base + (ti.m0 + r < ti.m ? ti.m0 + r : 0)];
-      }
+    for (int i = 0; i < C::LPP; ++i) {
+      const int r = 64 * wave + C::RPI * i + ln / C::CPR;
+      xr[i] = r;
+      if (a.x_rows) xr[i] = a.x_rows[ti.row_base + (ti.m0 + r < ti.m ? ti.m0 + r : 0)];
+    }
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = 16 * (4 * q + i) + (lane >> 2);
-        ld_off[i] = ti.m0 + r < ti.m ? static_cast<uint32_t>(xr[i] * a.K * 2 + chunk * 16) : kInvalid;
-      }
-    } else {
-      const int col0 = ti.nt * OUT_COLS;
-      // the wave's 64 weight rows 64q..64q+63 are all gate rows or all up rows
-      const bool up = GATED && (q & 1);
-      const uint16_t* wbase = (up ? a.w1 : a.w0) + static_cast<size_t>(ti.g) * a.group_stride +
-                              static_cast<size_t>(col0) * a.ldw;
-      rs_ld = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(wbase), 0, kRecords, kRsrcWord3);
+    for (int i = 0; i < C::LPP; ++i) {
+      const int r = 64 * wave + C::RPI * i + ln / C::CPR;
+      xoff[i] = (ti.m0 + r < ti.m ? static_cast<uint32_t>(xr[i] * a.K * 2 + ld_chunk_l(i, ln) * 16) : kInvalid) | dead;
+    }
+    const int col0 = ti.nt * OUT_COLS;
+    const size_t gofs = static_cast<size_t>(ti.g) * a.group_stride + static_cast<size_t>(col0) * a.ldw;
+    rs_w0 = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.w0 + gofs), 0, kRecords, kRsrcWord3);
+    if (GATED) rs_w1 = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a.w1 + gofs), 0, kRecords, kRsrcWord3);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = 16 * (4 * q + i) + (lane >> 2);            // weight row within the tile
-        const int lcol = GATED ? (r >> 7) * 64 + (r & 63) : r;  // output column relative to col0
-        ld_off[i] = (col0 + lcol < a.N) ? static_cast<uint32_t>(lcol * a.ldw * 2 + chunk * 16) : kInvalid;
-      }
+    for (int i = 0; i < C::LPP; ++i) {
+      const int r = 64 * wave + C::RPI * i + ln / C::CPR;  // weight row of the tile
+      const int lcol = GATED ? (r >> 7) * 64 + (r & 63) : r;
+      woff[i] = ((col0 + lcol < a.N) ? static_cast<uint32_t>(lcol * a.ldw * 2 + ld_chunk_l(i, ln) * 16) : kInvalid) | dead;
     }
   };
-  // Byte offset of the stage's K origin (added to every load's row-and-chunk
-  // offset) and the mark of a chunk past K.  The offset is the same for all
-  // lanes except for weights whose K range is stacked from segments that a
-  // 32-wide stage can straddle.
-  uint32_t ld_k = 0, ld_kmask = 0;
-  auto ld_kstep = [&]() {
-    const int k0 = ld_kb * kBK;
-    ld_kmask = k0 + chunk * 8 < a.K ? 0u : kInvalid;
-    if (grp == 0 || a.kseg >= a.K) {
-      ld_k = static_cast<uint32_t>(k0 * 2);
-    } else if (a.kseg % kBK == 0) {
+  // the 64 weight rows of this wave are all gate rows or all up rows
+  const bool w_up = GATED && (wave & 1);
+  // Per stage and lane: the K offset of X and of W and the past-K mark for
+  // the (at most two) chunks a lane fetches; p = load index parity.
+  uint32_t kx0 = 0, kx1 = 0, kw0 = 0, kw1 = 0;
+  auto kstep_one = [&](int p, uint32_t& kx, uint32_t& kw) {
+    const int k0 = ld_kb * C::BK;
+    const int ch = ld_chunk(p);
+    const uint32_t mask = k0 + ch * 8 < a.K ? 0u : kInvalid;
+    kx = static_cast<uint32_t>(k0 * 2) | mask;
+    uint32_t w;
+    if (a.kseg >= a.K) {
+      w = static_cast<uint32_t>(k0 * 2);
+    } else if (a.kseg % C::BK == 0) {
       const int seg = k0 / a.kseg;
-      ld_k = static_cast<uint32_t>((static_cast<size_t>(seg) * a.seg_stride + (k0 - seg * a.kseg)) * 2);
+      w = static_cast<uint32_t>((static_cast<size_t>(seg) * a.seg_stride + (k0 - seg * a.kseg)) * 2);
     } else {
-      const int kk = min(k0 + chunk * 8, a.K - 8);
-      ld_k = static_cast<uint32_t>((weight_col_offset(a, kk) - static_cast<size_t>(kk - k0)) * 2);
+      const int kk = min(k0 + ch * 8, a.K - 8);
+      w = static_cast<uint32_t>((weight_col_offset(a, kk) - static_cast<size_t>(kk - k0)) * 2);
+    }
+    kw = w | mask;
+  };
+  auto ld_kstep = [&]() {
+    kstep_one(0, kx0, kw0);
+    kstep_one(1, kx1, kw1);
+  };
+  // load l (0..LPS-1) of the stage being loaded into buffer buf: X loads first, then W
+  auto load_one = [&](int buf, int l) {
+    unsigned char* base = smem + buf * C::STAGE;
+    if (l < C::LPP) {
+      const uint32_t k = (l & 1) ? kx1 : kx0;
+      load_lds16(rs_x, base + wave * (64 * C::ROW) + l * 1024, (xoff[l] + k) | (k & kInvalid));
+    } else {
+      const int i = l - C::LPP;
+      const uint32_t k = (i & 1) ? kw1 : kw0;
+      load_lds16(w_up ? rs_w1 : rs_w0, base + C::PART + wave * (64 * C::ROW) + i * 1024,
+                 (woff[i] + k) | (k & kInvalid));
     }
   };
-  // load i (of 4) of this wave's part of the stage being loaded, into buffer buf
-  auto load_one = [&](int buf, int i) {
-    load_lds16(rs_ld, smem + buf * kStageBytes + grp * kPartBytes + q * 4096 + i * 1024,
-               (ld_off[i] + ld_k) | ld_kmask);
-  };
-  auto ld_advance = [&]() {  // after the four loads of a stage
+  auto ld_advance = [&]() {
     if (++ld_kb == nkb) {
       ld_kb = 0;
       ld_tile += gridDim.x;
@@ -254,56 +281,56 @@ __global__ __launch_bounds__(kThreads) void tiled_kernel(GemmArgs a) {
     }
     ld_kstep();
   };
-  auto issue = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) load_one(buf, i);
-    ld_advance();
-  };
 
-  // ---- compute side ----
-  const int xrow0 = grp * 128 + (q & 1) * 64;  // this wave's token rows in the tile
-  const int wrow0 = (q >> 1) * 128;            // and its weight rows
-  const int rsw = (lrow >> 2) & 3;             // slot key of the rows this lane reads
-  bf16x8 xf[2][2], wf[2][4];                   // [k-step][tile]
-  f32x16 acc[4][2];
-  auto read_frags = [&](int buf, int ks) {  // the fragments of one K-step
-    const unsigned char* b = smem + buf * kStageBytes;
-    {
-      const int slot = ((2 * ks + lhalf) ^ rsw) << 4;
+  // ---- compute side: token rows 128wm.., weight rows 128wn.. ----
+  const int xrow0 = wm * 128, wrow0 = wn * 128;
+  const int rsw = (lrow / C::SWZ) % C::CPR;
+  bf16x8 xf[2][4], wf[2][4];
+  f32x16 acc[4][4];
+  auto read_frags = [&](int buf, int ks, int set) {
+    const unsigned char* b = smem + buf * C::STAGE;
+    const int slot = ((2 * ks + lhalf) ^ rsw) << 4;
 #pragma unroll
-      for (int tn = 0; tn < 4; ++tn)
-        wf[ks][tn] = as_bf16x8(*reinterpret_cast<const u32x4*>(b + kPartBytes + (wrow0 + tn * 32 + lrow) * kRowBytes + slot));
-#pragma unroll
-      for (int tm = 0; tm < 2; ++tm)
-        xf[ks][tm] = as_bf16x8(*reinterpret_cast<const u32x4*>(b + (xrow0 + tm * 32 + lrow) * kRowBytes + slot));
+    for (int t = 0; t < 4; ++t) {
+      wf[set][t] = as_bf16x8(*reinterpret_cast<const u32x4*>(b + C::PART + (wrow0 + t * 32 + lrow) * C::ROW + slot));
+      xf[set][t] = as_bf16x8(*reinterpret_cast<const u32x4*>(b + (xrow0 + t * 32 + lrow) * C::ROW + slot));
     }
   };
-  auto mfma_step = [&](int ks) {
+  auto mfma_set = [&](int set) {
 #pragma unroll
     for (int tn = 0; tn < 4; ++tn)
 #pragma unroll
-      for (int tm = 0; tm < 2; ++tm) acc[tn][tm] = mfma32x32x16(wf[ks][tn], xf[ks][tm], acc[tn][tm]);
+      for (int tm = 0; tm < 4; ++tm) acc[tn][tm] = mfma32x32x16(wf[set][tn], xf[set][tm], acc[tn][tm]);
   };
   auto zero_acc = [&]() {
 #pragma unroll
     for (int tn = 0; tn < 4; ++tn)
 #pragma unroll
-      for (int tm = 0; tm < 2; ++tm) acc[tn][tm] = f32x16{};
+      for (int tm = 0; tm < 4; ++tm) acc[tn][tm] = f32x16{};
   };
-  // lane holds C[n = 8*(v/4) + 4*lhalf + v%4][t = lrow] of each 32x32 tile
+  // Lane (erow, ehalf) of a 32x32 accumulator tile holds row erow, columns
+  // 8*v4 + 4*ehalf + 0..3.  Values go out in bf16 pairs; a swap between the
+  // lane halves gives every lane 8 consecutive columns, one 16-byte store.
   auto epilogue = [&](const TileInfo& ti) {
+    // an opaque copy of the lane id keeps the compiler from hoisting the
+    // epilogue's per-lane addresses out of the K loop (they would hold
+    // registers through it)
+    int ln = opaque_lane_id();
+    const int erow = ln & 31, ehalf = ln >> 5;
+    constexpr int WCOLS = GATED ? 64 : 128;  // output columns of this wave
+    const int col_w = ti.nt * OUT_COLS + wn * WCOLS;
+    const bool cols_full = col_w + WCOLS <= a.N;
 #pragma unroll
-    for (int tm = 0; tm < 2; ++tm) {
-      const int row = ti.m0 + xrow0 + tm * 32 + lrow;
-      if (row >= ti.m) continue;
-      uint16_t* orow = a.out + static_cast<size_t>(ti.row_base + row) * a.N;
+    for (int tm = 0; tm < 4; ++tm) {
+      const int row = ti.m0 + xrow0 + tm * 32 + erow;
+      const bool row_ok = row < ti.m;
+      uint16_t* orow = a.out + static_cast<size_t>(ti.row_base + (row_ok ? row : 0)) * a.N;
       constexpr int TOUT = GATED ? 2 : 4;
 #pragma unroll
       for (int tn = 0; tn < TOUT; ++tn) {
+        uint32_t pk[8];  // pk[2*v4 + h]: columns 8*v4 + 4*ehalf + 2h, +1
 #pragma unroll
         for (int v4 = 0; v4 < 4; ++v4) {
-          const int col = ti.nt * OUT_COLS + (q >> 1) * (GATED ? 64 : 128) + tn * 32 + 8 * v4 + 4 * lhalf;
-          if (col >= a.N) continue;
           float o[4];
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
@@ -313,68 +340,88 @@ __global__ __launch_bounds__(kThreads) void tiled_kernel(GemmArgs a) {
             else
               o[i] = c0;
           }
-          uint2 pk;
-          pk.x = pack_bf16x2(o[0], o[1]);
-          pk.y = pack_bf16x2(o[2], o[3]);
-          *reinterpret_cast<uint2*>(orow + col) = pk;
+          pk[2 * v4] = cvt_pk_bf16(o[0], o[1]);
+          pk[2 * v4 + 1] = cvt_pk_bf16(o[2], o[3]);
+        }
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {  // columns 16q .. 16q+15 of the 32-column tile
+          // lower lanes keep columns 16q+0..3 and take 16q+4..7 from the upper
+          // half; upper lanes take 16q+8..11 and keep 16q+12..15
+          const auto s0 = __builtin_amdgcn_permlane32_swap(pk[4 * q], pk[4 * q + 2], false, false);
+          const auto s1 = __builtin_amdgcn_permlane32_swap(pk[4 * q + 1], pk[4 * q + 3], false, false);
+          const u32x4 v = {s0[0], s1[0], s0[1], s1[1]};
+          const int col = col_w + tn * 32 + 16 * q + 8 * ehalf;
+          if (row_ok && (cols_full || col < a.N)) *reinterpret_cast<u32x4*>(orow + col) = v;
         }
       }
     }
   };
 
   // ---- pipeline ----
-  TileInfo cur = tile_info(first);
-  int cur_tile = first, kb = 0;
+  // The barrier of stage j sits before its last K-step, after every wave's
+  // last LDS read of stage j: from then on stage j's buffer takes the loads
+  // of stage j + NS.  Their first half is issued among the MFMAs of stage
+  // j's last K-step, the second half among those of stage j + 1's first
+  // K-step, one load per four MFMAs: a burst of loads stalls the issuing wave
+  // (one wave per SIMD) while the address unit drains, and the MFMA pipe with
+  // it.  Stage j + 1 must have landed by the barrier of stage j.
+  constexpr int H1 = C::LPS / 2;  // loads of a stage issued in its first slot
   zero_acc();
   ld_setup(first);
   ld_kstep();
-  issue(0);
-  issue(1);
-  issue(2);
-  __builtin_amdgcn_s_waitcnt(wait_vm(2 * kLoadsPerStage));  // own stage-0 loads landed
-  phase_barrier();
-  if (grp == 1) phase_barrier();  // group 1 runs one phase behind
-  for (int j = 0; j < n_stages; ++j) {
-    // memory phase of stage j
-    if (kb == 0 && j > 0) {
-      epilogue(cur);
-      zero_acc();
-      cur_tile += gridDim.x;
-      cur = tile_info(cur_tile);
-    }
-    // The stage's four loads are spread over both phases, between the LDS
-    // reads and between the MFMAs: the texture unit takes them one by one
-    // and no wave stalls on a burst of loads.
-    const int lb = (j + 3) & 3;
-    load_one(lb, 0);
-    read_frags(j & 3, 0);
-    load_one(lb, 1);
-    read_frags(j & 3, 1);
-    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
-    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
-    if (grp == 1) __builtin_amdgcn_s_waitcnt(wait_vm(kLoadsPerStage + 2));  // own stage j+1 landed
-    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
-    phase_barrier();
-    // compute phase of stage j
-    mfma_step(0);
-    load_one(lb, 2);
-    mfma_step(1);
-    load_one(lb, 3);
-    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-    if (grp == 0) __builtin_amdgcn_s_waitcnt(wait_vm(2 * kLoadsPerStage));  // own stage j+1 landed
-    phase_barrier();
-    ld_advance();
-    if (++kb == nkb) kb = 0;
+  for (int s = 0; s < C::NS; ++s) {
+    const int n = s + 1 < C::NS ? C::LPS : H1;
+    for (int l = 0; l < n; ++l) load_one(s, l);
+    if (s + 1 < C::NS) ld_advance();
   }
-  if (grp == 0) phase_barrier();  // matches group 1's extra barrier
-  epilogue(cur);
-  __builtin_amdgcn_s_waitcnt(kWaitAll);  // no load may land in LDS after the workgroup ends
+  // in flight: stages 0 .. NS-2 whole and the first half of stage NS - 1
+  __builtin_amdgcn_s_waitcnt(wait_vm((C::NS - 2) * C::LPS + H1));  // own stage-0 loads landed
+  phase_barrier();
+  read_frags(0, 0, 0);
+  int j = 0;
+  for (int t = first; t < total_tiles; t += gridDim.x) {
+    for (int kb = 0; kb < nkb; ++kb, ++j) {
+      const int buf = j & (C::NS - 1);
+      const int pbuf = (j + C::NS - 1) & (C::NS - 1);  // stage j + NS - 1 (= buffer of j - 1)
+      // K-step 0: the second half of stage j + NS - 1's loads among its MFMAs
+      read_frags(buf, 1, 1);
+#pragma unroll
+      for (int l = H1; l < C::LPS; ++l) load_one(pbuf, l);
+      mfma_set(0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+      for (int l = H1; l < C::LPS; ++l) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 16 / (C::LPS - H1), 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      ld_advance();  // to stage j + NS
+#pragma unroll
+      for (int ks = 1; ks < C::KSTEPS - 1; ++ks) {
+        read_frags(buf, ks + 1, (ks + 1) & 1);
+        mfma_set(ks & 1);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_waitcnt(wait_vm((C::NS - 2) * C::LPS));  // own stage j+1 landed
+      __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+      phase_barrier();
+      // last K-step: the first half of stage j + NS's loads among its MFMAs
+      read_frags((j + 1) & (C::NS - 1), 0, 0);  // past the last stage: a harmless stale read
+#pragma unroll
+      for (int l = 0; l < H1; ++l) load_one(buf, l);
+      mfma_set((C::KSTEPS - 1) & 1);
+      __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+      for (int l = 0; l < H1; ++l) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 16 / H1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    epilogue(tile_info(t));
+    zero_acc();
+  }
+  __builtin_amdgcn_s_waitcnt(kWaitAll);
 }
 
 int device_cu_count() {
@@ -396,7 +443,7 @@ hipError_t launch_tiled_t(const Segments& seg, const GemmArgs& a, hipStream_t st
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&tiled_kernel<GATED>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes);
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, Stage::LDS);
     if (e != hipSuccess) return e;
     attr_set = true;
   }
@@ -406,7 +453,7 @@ hipError_t launch_tiled_t(const Segments& seg, const GemmArgs& a, hipStream_t st
   if (tiles == 0) return hipSuccess;
   long long grid = std::min<long long>(tiles, device_cu_count());  // one workgroup per CU (LDS)
   grid = ((grid + 7) / 8) * 8;
-  hipLaunchKernelGGL((tiled_kernel<GATED>), dim3(static_cast<unsigned>(grid)), dim3(kThreads), kLdsBytes, st, a);
+  hipLaunchKernelGGL((tiled_kernel<GATED>), dim3(static_cast<unsigned>(grid)), dim3(kThreads), Stage::LDS, st, a);
   return hipGetLastError();
 }
 
