@@ -341,16 +341,20 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
     const int erow = ln & 31, ehalf = ln >> 5;
     constexpr int WCOLS = GATED ? 64 : 128;
     const int col_w = ti.nt * OUT_COLS + wn * WCOLS;
-    const bool cols_full = col_w + WCOLS <= a.N;
+    // The tile's output rows through a buffer descriptor: rows past the
+    // group and columns past N get offsets >= 2^31, which the hardware
+    // drops, so the stores need no branches and the conversions of all of
+    // a row group's tiles can overlap.
+    const __amdgpu_buffer_rsrc_t rs_o = __builtin_amdgcn_make_buffer_rsrc(
+        a.out + static_cast<size_t>(ti.row_base + ti.m0) * a.N, 0, kRecords, kRsrcWord3);
 #pragma unroll
     for (int tm = 0; tm < 4; ++tm) {
-      const int row = ti.m0 + xrow0 + tm * 32 + erow;
-      const bool row_ok = row < ti.m;
-      uint16_t* orow = a.out + static_cast<size_t>(ti.row_base + (row_ok ? row : 0)) * a.N;
+      const int r = xrow0 + tm * 32 + erow;  // row within the tile
+      const uint32_t row_off = ti.m0 + r < ti.m ? static_cast<uint32_t>(r * a.N * 2) : kInvalid;
       constexpr int TOUT = GATED ? 2 : 4;
 #pragma unroll
       for (int tn = 0; tn < TOUT; ++tn) {
-        uint32_t pk[8];
+        uint32_t pk[8];  // pk[2*v4 + h]: columns 8*v4 + 4*ehalf + 2h, +1
 #pragma unroll
         for (int v4 = 0; v4 < 4; ++v4) {
           float o[4];
@@ -366,12 +370,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
           pk[2 * v4 + 1] = cvt_pk_bf16(o[2], o[3]);
         }
 #pragma unroll
-        for (int q = 0; q < 2; ++q) {
+        for (int q = 0; q < 2; ++q) {  // columns 16q .. 16q+15 of the 32-column tile
+          // lower lanes keep columns 16q+0..3 and take 16q+4..7 from the upper
+          // half; upper lanes take 16q+8..11 and keep 16q+12..15
           const auto s0 = __builtin_amdgcn_permlane32_swap(pk[4 * q], pk[4 * q + 2], false, false);
           const auto s1 = __builtin_amdgcn_permlane32_swap(pk[4 * q + 1], pk[4 * q + 3], false, false);
           const u32x4 v = {s0[0], s1[0], s0[1], s1[1]};
           const int col = col_w + tn * 32 + 16 * q + 8 * ehalf;
-          if (row_ok && (cols_full || col < a.N)) *reinterpret_cast<u32x4*>(orow + col) = v;
+          const uint32_t off = col < a.N ? row_off + static_cast<uint32_t>(col * 2) : kInvalid;
+          __builtin_amdgcn_raw_buffer_store_b128(v, rs_o, off | (row_off & kInvalid), 0, 0);
         }
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -499,12 +506,13 @@ hipError_t launch_tiled_t(const Segments& seg, const GemmArgs& a, hipStream_t st
 
 hipError_t launch_tiled(const Segments& seg, const GemmArgs& a, bool gated, hipStream_t st) {
   if (seg.groups > kMaxGroups || a.x_blocked || a.out_blocked) return hipErrorInvalidValue;
-  // 32-bit byte offsets: a tile's X rows (all of x when rows are indexed) and
-  // a group's weight columns
+  // 32-bit byte offsets: a tile's X rows (all of x when rows are indexed), a
+  // group's weight columns and a tile's output rows
   const size_t x_span = static_cast<size_t>(a.x_rows ? a.x_row_count : kBM) * a.K * 2;
   const size_t w_span = (static_cast<size_t>(kBN) * a.ldw +
                          (a.kseg < a.K ? static_cast<size_t>((a.K - 1) / a.kseg) * a.seg_stride : 0) + a.K) * 2;
-  if (x_span >= 0x80000000ull || w_span >= 0x80000000ull) return hipErrorInvalidValue;
+  const size_t o_span = static_cast<size_t>(kBM + 1) * a.N * 2;
+  if (x_span >= 0x80000000ull || w_span >= 0x80000000ull || o_span >= 0x80000000ull) return hipErrorInvalidValue;
   return gated ? launch_tiled_t<true>(seg, a, st) : launch_tiled_t<false>(seg, a, st);
 }
 
