@@ -14,10 +14,12 @@
 // groups that end at or before the tile.  Group sizes never leave the
 // device.
 //
-// Waves.  Four waves, one per SIMD; wave (wm, wn) owns token rows
-// 128*wm .. +127 and weight rows 128*wn .. +127 of the tile: 4 x 4
+// Waves.  Eight waves, two per SIMD; wave (wm, wn) owns token rows
+// 64*wm .. +63 and weight rows 128*wn .. +127 of the tile: 2 x 4
 // v_mfma_f32_32x32x16_bf16 tiles (weights as the A operand, tokens as B),
-// 256 fp32 accumulators held in AGPRs.
+// 128 fp32 accumulators.  Two waves per SIMD let one wave's MFMAs run while
+// the other waits to issue a load: with one wave per SIMD (128 x 128 each,
+// half the LDS reads per MFMA) the MFMA pipe idled during every such stall.
 //
 // Stages.  K advances in stages of 64.  A stage is an X part [256 x 64] and
 // a W part [256 x 64] (128-byte rows, 32 KB each), filled by
@@ -38,8 +40,8 @@
 // LDS reads: past barrier j the slot of X of stage j takes W of stage j + 2
 // (issued among the MFMAs of stage j's last K-step and stage j + 1's first)
 // and the slot of W of stage j takes X of stage j + 3 (issued among the
-// MFMAs of stage j + 1's K-steps 1 and 2): four loads per K-step, one per
-// four MFMAs.  A burst of loads stalls the issuing wave (one wave per SIMD,
+// MFMAs of stage j + 1's K-steps 1 and 2): two loads per wave and K-step,
+// one per four MFMAs.  A burst of loads stalls the issuing wave (one wave per SIMD,
 // in order) while the address unit drains, and the MFMA pipe with it.  The
 // stage sequence runs on across tile boundaries.
 //
@@ -54,7 +56,7 @@ namespace {
 
 constexpr int kBM = 256;             // token rows per tile
 constexpr int kBN = 256;             // weight rows per tile
-constexpr int kThreads = 4 * kWave;  // four waves, one per SIMD
+constexpr int kThreads = 8 * kWave;  // eight waves, two per SIMD
 constexpr int kMaxGroups = 1024;
 
 // One K stage and the ring of its parts.
@@ -67,7 +69,7 @@ struct Stage {
   static constexpr int PART = kBM * ROW;     // one operand of a stage: 32 KB
   static constexpr int NPARTS = 5;           // ring slots
   static constexpr int LDS = NPARTS * PART;  // 160 KB, all of it
-  static constexpr int LPP = 64 / RPI;       // loads per part per wave
+  static constexpr int LPP = 32 / RPI;       // loads per part per wave
   static constexpr int KSTEPS = BK / 16;     // MFMA K-steps per stage
 };
 static_assert(kBM == kBN && Stage::RPI * Stage::ROW == 1024, "a load fills 1 KB of LDS rows");
@@ -117,7 +119,7 @@ __device__ __forceinline__ int wave_min(int v) {
 }
 
 template <bool GATED, int kPfx>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) void tiled_kernel(GemmArgs a) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void tiled_kernel(GemmArgs a) {
   using C = Stage;
   constexpr int OUT_COLS = GATED ? kBN / 2 : kBN;
   constexpr uint32_t kInvalid = 0x80000000u;
@@ -129,7 +131,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
-  const int wm = wave & 1, wn = wave >> 1;
+  const int wm = wave & 3, wn = wave >> 2;
   const int lrow = lane & 31, lhalf = lane >> 5;
   const int n_tiles_n = ceil_div(a.N, OUT_COLS);
 
@@ -208,14 +210,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
   };
 
   // ---- load side ----
-  // Two streams, X one stage ahead of W.  Wave w fills rows 64w..64w+63 of
-  // a part; load i writes rows 64w + 8i + lane/8, slot lane%8, fetching
+  // Two streams, X one stage ahead of W.  Wave w fills rows 32w..32w+31 of
+  // a part; load i writes rows 32w + 8i + lane/8, slot lane%8, fetching
   // the global chunk slot ^ ((row / 2) % 8).
   auto chunk_of = [&](int i, int ln) {
-    const int r = 64 * wave + C::RPI * i + ln / C::CPR;
+    const int r = 32 * wave + C::RPI * i + ln / C::CPR;
     return (ln % C::CPR) ^ ((r / C::SWZ) % C::CPR);
   };
-  const bool w_up = GATED && (wave & 1);
+  // the 32 weight rows of this wave are all gate rows or all up rows
+  const bool w_up = GATED && ((wave >> 1) & 1);
   __amdgpu_buffer_rsrc_t rs_x, rs_w;
   uint32_t xoff[C::LPP], woff[C::LPP];
   int x_tile = first, x_kb = 0, w_tile = first, w_kb = 0;
@@ -232,13 +235,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
     int xr[C::LPP];
 #pragma unroll
     for (int i = 0; i < C::LPP; ++i) {
-      const int r = 64 * wave + C::RPI * i + ln / C::CPR;
+      const int r = 32 * wave + C::RPI * i + ln / C::CPR;
       xr[i] = r;
       if (a.x_rows) xr[i] = a.x_rows[ti.row_base + (ti.m0 + r < ti.m ? ti.m0 + r : 0)];
     }
 #pragma unroll
     for (int i = 0; i < C::LPP; ++i) {
-      const int r = 64 * wave + C::RPI * i + ln / C::CPR;
+      const int r = 32 * wave + C::RPI * i + ln / C::CPR;
       xoff[i] = (ti.m0 + r < ti.m ? static_cast<uint32_t>(xr[i] * a.K * 2 + chunk_of(i, ln) * 16) : kInvalid) | dead;
     }
   };
@@ -253,7 +256,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
     rs_w = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>((w_up ? a.w1 : a.w0) + gofs), 0, kRecords, kRsrcWord3);
 #pragma unroll
     for (int i = 0; i < C::LPP; ++i) {
-      const int r = 64 * wave + C::RPI * i + ln / C::CPR;
+      const int r = 32 * wave + C::RPI * i + ln / C::CPR;
       const int lcol = GATED ? (r >> 7) * 64 + (r & 63) : r;
       woff[i] = ((col0 + lcol < a.N) ? static_cast<uint32_t>(lcol * a.ldw * 2 + chunk_of(i, ln) * 16) : kInvalid) | dead;
     }
@@ -302,39 +305,40 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
   auto part_ptr = [&](int P) { return smem + (P % C::NPARTS) * C::PART; };
   auto x_load = [&](int s, int i) {
     const uint32_t k = (i & 1) ? kx1 : kx0;
-    load_lds16(rs_x, part_ptr(2 * s) + wave * (64 * C::ROW) + i * 1024, (xoff[i] + k) | (k & kInvalid));
+    load_lds16(rs_x, part_ptr(2 * s) + wave * (32 * C::ROW) + i * 1024, (xoff[i] + k) | (k & kInvalid));
   };
   auto w_load = [&](int s, int i) {
     const uint32_t k = (i & 1) ? kw1 : kw0;
-    load_lds16(rs_w, part_ptr(2 * s + 1) + wave * (64 * C::ROW) + i * 1024, (woff[i] + k) | (k & kInvalid));
+    load_lds16(rs_w, part_ptr(2 * s + 1) + wave * (32 * C::ROW) + i * 1024, (woff[i] + k) | (k & kInvalid));
   };
 
   // ---- compute side ----
-  const int xrow0 = wm * 128, wrow0 = wn * 128;
+  const int xrow0 = wm * 64, wrow0 = wn * 128;
   const int rsw = (lrow / C::SWZ) % C::CPR;
-  bf16x8 xf[2][4], wf[2][4];
-  f32x16 acc[4][4];
+  bf16x8 xf[2][2], wf[2][4];
+  f32x16 acc[4][2];
   auto read_frags = [&](int s, int ks, int set) {
     const unsigned char* xp = part_ptr(2 * s);
     const unsigned char* wp = part_ptr(2 * s + 1);
     const int slot = ((2 * ks + lhalf) ^ rsw) << 4;
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
+    for (int t = 0; t < 4; ++t)
       wf[set][t] = as_bf16x8(*reinterpret_cast<const u32x4*>(wp + (wrow0 + t * 32 + lrow) * C::ROW + slot));
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
       xf[set][t] = as_bf16x8(*reinterpret_cast<const u32x4*>(xp + (xrow0 + t * 32 + lrow) * C::ROW + slot));
-    }
   };
   auto mfma_set = [&](int set) {
 #pragma unroll
     for (int tn = 0; tn < 4; ++tn)
 #pragma unroll
-      for (int tm = 0; tm < 4; ++tm) acc[tn][tm] = mfma32x32x16(wf[set][tn], xf[set][tm], acc[tn][tm]);
+      for (int tm = 0; tm < 2; ++tm) acc[tn][tm] = mfma32x32x16(wf[set][tn], xf[set][tm], acc[tn][tm]);
   };
   auto zero_acc = [&]() {
 #pragma unroll
     for (int tn = 0; tn < 4; ++tn)
 #pragma unroll
-      for (int tm = 0; tm < 4; ++tm) acc[tn][tm] = f32x16{};
+      for (int tm = 0; tm < 2; ++tm) acc[tn][tm] = f32x16{};
   };
   auto epilogue = [&](const TileInfo& ti) {
     const int ln = opaque_lane_id();
@@ -348,7 +352,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
     const __amdgpu_buffer_rsrc_t rs_o = __builtin_amdgcn_make_buffer_rsrc(
         a.out + static_cast<size_t>(ti.row_base + ti.m0) * a.N, 0, kRecords, kRsrcWord3);
 #pragma unroll
-    for (int tm = 0; tm < 4; ++tm) {
+    for (int tm = 0; tm < 2; ++tm) {
       const int r = xrow0 + tm * 32 + erow;  // row within the tile
       const uint32_t row_off = ti.m0 + r < ti.m ? static_cast<uint32_t>(r * a.N * 2) : kInvalid;
       constexpr int TOUT = GATED ? 2 : 4;
@@ -417,7 +421,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
     const TileInfo cur = tile_info(t);  // scalars, held through the K loop
     for (int kb = 0; kb < nkb; ++kb, ++j) {
       // K-step 0 with the second half of W of stage j + 1, K-steps 1 and 2
-      // with X of stage j + 2: four loads per K-step, one per four MFMAs
+      // with X of stage j + 2: two loads per wave and K-step, one per four MFMAs
 #pragma unroll
       for (int ks = 0; ks < C::KSTEPS - 1; ++ks) {
         read_frags(j, ks + 1, (ks + 1) & 1);
@@ -430,7 +434,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
         }
         if (ks == 0) w_advance();
         mfma_set(ks & 1);
-        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
 #pragma unroll
         for (int i = 0; i < C::LPP / 2; ++i) {
           __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
@@ -447,7 +451,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
 #pragma unroll
       for (int i = 0; i < C::LPP / 2; ++i) w_load(j + 2, i);
       mfma_set((C::KSTEPS - 1) & 1);
-      __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
 #pragma unroll
       for (int i = 0; i < C::LPP / 2; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
