@@ -40,9 +40,7 @@
 // LDS reads: past barrier j the slot of X of stage j takes W of stage j + 2
 // (issued among the MFMAs of stage j's last K-step and stage j + 1's first)
 // and the slot of W of stage j takes X of stage j + 3 (issued among the
-// MFMAs of stage j + 1's K-steps 1 and 2): two loads per wave and K-step,
-// one per four MFMAs.  A burst of loads stalls the issuing wave (one wave per SIMD,
-// in order) while the address unit drains, and the MFMA pipe with it.  The
+// MFMAs of stage j + 1's K-steps 1 and 2): two loads per wave and K-step.  The
 // stage sequence runs on across tile boundaries.
 //
 // Epilogue.  A lane holds row r, columns 8*v + 4*h + 0..3 (v < 4, h = lane
@@ -421,7 +419,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const TileInfo cur = tile_info(t);  // scalars, held through the K loop
     for (int kb = 0; kb < nkb; ++kb, ++j) {
       // K-step 0 with the second half of W of stage j + 1, K-steps 1 and 2
-      // with X of stage j + 2: two loads per wave and K-step, one per four MFMAs
+      // with X of stage j + 2: two loads per wave and K-step
 #pragma unroll
       for (int ks = 0; ks < C::KSTEPS - 1; ++ks) {
         read_frags(j, ks + 1, (ks + 1) & 1);
@@ -434,12 +432,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         }
         if (ks == 0) w_advance();
         mfma_set(ks & 1);
-        __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
-#pragma unroll
-        for (int i = 0; i < C::LPP / 2; ++i) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-          __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-        }
         __builtin_amdgcn_sched_barrier(0);
       }
       x_advance();
@@ -451,12 +443,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
       for (int i = 0; i < C::LPP / 2; ++i) w_load(j + 2, i);
       mfma_set((C::KSTEPS - 1) & 1);
-      __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
-#pragma unroll
-      for (int i = 0; i < C::LPP / 2; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-      }
       __builtin_amdgcn_sched_barrier(0);
     }
     epilogue(cur);
