@@ -1,5 +1,5 @@
 // Expert FFN for prefill-sized batches: a persistent bf16 MFMA grouped GEMM
-// with direct-to-LDS loads, one wave per SIMD.
+// with direct-to-LDS loads, two waves per SIMD.
 //
 // Tiles.  An output tile is 256 token rows x 256 weight rows of one group
 // (expert).  For the gate/up GEMM the 256 weight rows are 128 gate rows and
