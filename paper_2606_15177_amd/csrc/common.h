@@ -58,4 +58,19 @@ __device__ __forceinline__ f32x16 mfma32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// Host side: raise a kernel's dynamic LDS limit once per device.  The
+// attribute belongs to the current device's context, so a process that
+// drives several GPUs sets it on each; `done` is the kernel's bit mask of
+// devices already set (updated atomically, so concurrent callers are safe).
+inline hipError_t set_max_dynamic_lds(const void* kernel, int bytes, unsigned long long* done) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const unsigned long long bit = dev >= 0 && dev < 64 ? 1ull << dev : 0ull;
+  if (bit != 0 && (__atomic_load_n(done, __ATOMIC_ACQUIRE) & bit) != 0) return hipSuccess;
+  e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (e == hipSuccess && bit != 0) __atomic_fetch_or(done, bit, __ATOMIC_RELEASE);
+  return e;
+}
+
 }  // namespace moe

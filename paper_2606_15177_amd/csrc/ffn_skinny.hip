@@ -241,13 +241,11 @@ hipError_t launch_skinny_t(const Segments& seg, const GemmArgs& a, hipStream_t s
   constexpr size_t kLds = kRing > kRed ? kRing : kRed;
   static_assert(kLds <= 160 * 1024, "LDS");
   constexpr int WG_ROWS = GATED ? 32 : 32 * NB;
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&skinny_kernel<GATED, NB, KP, KS, DEPTH>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kLds));
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
+  static unsigned long long lds_set = 0;  // devices with the LDS limit raised
+  const hipError_t e_lds =
+      set_max_dynamic_lds(reinterpret_cast<const void*>(&skinny_kernel<GATED, NB, KP, KS, DEPTH>),
+                          static_cast<int>(kLds), &lds_set);
+  if (e_lds != hipSuccess) return e_lds;
   dim3 grid(ceil_div(a.N, WG_ROWS), seg.groups);
   hipLaunchKernelGGL((skinny_kernel<GATED, NB, KP, KS, DEPTH>), grid, dim3(KP * kWave), kLds, st, a);
   return hipGetLastError();

@@ -466,13 +466,11 @@ int device_cu_count() {
 
 template <bool GATED, int PFX>
 hipError_t launch_pfx(const GemmArgs& a, long long grid, hipStream_t st) {
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&tiled_kernel<GATED, PFX>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, Stage::LDS);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
+  static unsigned long long lds_set = 0;  // devices with the LDS limit raised
+  const hipError_t e_lds =
+      set_max_dynamic_lds(reinterpret_cast<const void*>(&tiled_kernel<GATED, PFX>),
+                          Stage::LDS, &lds_set);
+  if (e_lds != hipSuccess) return e_lds;
   hipLaunchKernelGGL((tiled_kernel<GATED, PFX>), dim3(static_cast<unsigned>(grid)), dim3(kThreads), Stage::LDS, st, a);
   return hipGetLastError();
 }

@@ -453,13 +453,11 @@ hipError_t launch_place(const PlaceArgs& h, hipStream_t st) {
   a.chunk = place_chunk_experts(h.S, h.E, h.G);
   for (int g = 0; g < h.G; ++g) a.cap[g] = h.cap[g];
   const size_t lds = place_lds_bytes(h.S, h.E, h.G);
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&place_kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, kPlaceMaxLdsBytes);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
+  static unsigned long long lds_set = 0;  // devices with the LDS limit raised
+  const hipError_t e_lds =
+      set_max_dynamic_lds(reinterpret_cast<const void*>(&place_kernel),
+                          kPlaceMaxLdsBytes, &lds_set);
+  if (e_lds != hipSuccess) return e_lds;
   hipLaunchKernelGGL(place_kernel, dim3(h.L), dim3(kPlaceThreads), lds, st, a);
   return hipGetLastError();
 }

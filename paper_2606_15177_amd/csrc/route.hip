@@ -316,13 +316,11 @@ hipError_t launch_route_gv(const RouteKernelArgs& in, hipStream_t st) {
   a.lds_bins = (a.counts && a.S * a.E <= kLdsBinsMax) ? a.S * a.E : 0;
   const size_t lds = a.lds_bins * sizeof(int) + ((EXT && a.n_group > 1) ? sizeof(float) * kGroups * a.E : 0);
   if (EXT) {
-    static bool attr_set = false;
-    if (!attr_set) {
-      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&route_kernel<G, V, EXT>),
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
-      if (e != hipSuccess) return e;
-      attr_set = true;
-    }
+    static unsigned long long lds_set = 0;  // devices with the LDS limit raised
+    const hipError_t e_lds =
+        set_max_dynamic_lds(reinterpret_cast<const void*>(&route_kernel<G, V, EXT>),
+                            160 * 1024, &lds_set);
+    if (e_lds != hipSuccess) return e_lds;
   }
   hipLaunchKernelGGL((route_kernel<G, V, EXT>), dim3(blocks), dim3(kBlock), lds, st, a);
   return hipGetLastError();
