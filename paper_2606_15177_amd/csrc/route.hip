@@ -326,19 +326,43 @@ hipError_t launch_route_gv(const RouteKernelArgs& in, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <int G, bool EXT>
+hipError_t launch_route_g(const RouteKernelArgs& a, int V, hipStream_t st) {
+  switch (V) {
+    case 1: return launch_route_gv<G, 1, EXT>(a, st);
+    case 2: return launch_route_gv<G, 2, EXT>(a, st);
+    case 4: return launch_route_gv<G, 4, EXT>(a, st);
+    case 8: return launch_route_gv<G, 8, EXT>(a, st);
+    default: return launch_route_gv<G, 16, EXT>(a, st);
+  }
+}
+
+// Lanes per token G and logits per lane V: G covers E when E <= 16;
+// otherwise the narrowest G >= 16 that holds the picks (k) and the expert
+// groups (one lane each), with at most 8 logits per lane below 1024 experts.
+// Narrow groups route more tokens per wave, and a max over 16 lanes is four
+// DPP steps within a row.
 template <bool EXT>
 hipError_t launch_route_ext(const RouteKernelArgs& a, hipStream_t st) {
   const int E = a.E;
-  if (E <= 2) return launch_route_gv<2, 1, EXT>(a, st);
-  if (E <= 4) return launch_route_gv<4, 1, EXT>(a, st);
-  if (E <= 8) return launch_route_gv<8, 1, EXT>(a, st);
-  if (E <= 16) return launch_route_gv<16, 1, EXT>(a, st);
-  if (E <= 32) return launch_route_gv<32, 1, EXT>(a, st);
-  if (E <= 64) return launch_route_gv<64, 1, EXT>(a, st);
-  if (E <= 128) return launch_route_gv<64, 2, EXT>(a, st);
-  if (E <= 256) return launch_route_gv<64, 4, EXT>(a, st);
-  if (E <= 512) return launch_route_gv<64, 8, EXT>(a, st);
-  return launch_route_gv<64, 16, EXT>(a, st);
+  const int need = max(a.k, EXT && a.n_group > 1 ? a.n_group : 1);
+  int G = 2;
+  if (E <= 16) {
+    while (G < E) G *= 2;
+  } else {
+    G = 16;
+    while (G < 64 && (G < need || E > 8 * G)) G *= 2;
+  }
+  int V = 1;
+  while (V * G < E) V *= 2;
+  switch (G) {
+    case 2: return launch_route_g<2, EXT>(a, V, st);
+    case 4: return launch_route_g<4, EXT>(a, V, st);
+    case 8: return launch_route_g<8, EXT>(a, V, st);
+    case 16: return launch_route_g<16, EXT>(a, V, st);
+    case 32: return launch_route_g<32, EXT>(a, V, st);
+    default: return launch_route_g<64, EXT>(a, V, st);
+  }
 }
 
 }  // namespace
