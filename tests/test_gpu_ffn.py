@@ -75,6 +75,8 @@ def _run_ffn(moe, cfg, wl, idx):
     (2048, 128, 128, 8, 128, 128, 0, 0),     # 65..256 groups
     (4096, 128, 300, 8, 128, 300, 0, 0),     # 257..1024 groups
     (8192, 64, 1024, 8, 64, 1024, 0, 0),     # the largest group count
+    (600, 16, 4, 2, 8, 4, 0, 0),             # one partial K stage, a partial column tile
+    (520, 24, 2, 1, 24, 2, 1, 16),           # small shared expert next to the routed ones
 ])
 def test_ffn_paths(moe, T, H, E, k, I, E_local, n_sh, I_sh):
     cfg, wl, idx = _case(T, H, E, k, I, E_local, n_sh, I_sh)
