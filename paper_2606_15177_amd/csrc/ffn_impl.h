@@ -12,8 +12,7 @@ namespace moe {
 // (c / kseg)*seg_stride + c % kseg for K stacked over several experts.
 // GATED kernels read two such matrices (w0 = gate, w1 = up) and write
 // silu(gate) * up.  x rows have stride K and out rows stride N; row r of the
-// grouped activation matrix is x[x_rows[r]] when x_rows != nullptr
-// (weight-streaming kernel only).
+// grouped activation matrix is x[x_rows[r]] when x_rows != nullptr.
 //
 // Chunk-blocked layout (weight-streaming kernel with device offsets only, K
 // and N multiples of 16): a group's rows are cut into chunks of 32, the last
