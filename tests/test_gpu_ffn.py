@@ -102,6 +102,16 @@ def test_ffn_group_larger_than_batch(moe):
     assert _run_ffn(moe, cfg, wl, idx) == 2 * T
 
 
+def test_ffn_tile_boundaries(moe):
+    """Groups of 1, 127..129, 255..257 and 511..513 rows: one row, half and
+    whole 256-row m-tiles, and one row past them, side by side in one launch."""
+    sizes = [1, 127, 128, 129, 255, 256, 257, 511, 512, 513, 65]
+    T = sum(sizes)
+    cfg, wl, _ = _case(T, 136, len(sizes), 1, 200, len(sizes))
+    idx = np.repeat(np.arange(len(sizes), dtype=np.int32), sizes)[np.random.default_rng(3).permutation(T)]
+    assert _run_ffn(moe, cfg, wl, idx.reshape(T, 1)) == T
+
+
 def _combine(moe, T, k, H, R, with_shared, seed):
     rng = np.random.default_rng(seed)
     y = W.f32_to_bf16_bits(rng.standard_normal((max(R, 1), H)).astype(np.float32))
