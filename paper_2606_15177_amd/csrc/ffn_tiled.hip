@@ -14,6 +14,11 @@
 // groups that end at or before the tile.  Group sizes never leave the
 // device.
 //
+// Two problems.  The shared experts (static rows: every token) can run in
+// the routed experts' launch: their tiles come first, and each load stream
+// and the epilogue follow the problem of the tile they are on.  This is used
+// when the shared tiles alone would leave a partly filled last round.
+//
 // Waves.  Eight waves, two per SIMD; wave (wm, wn) owns token rows
 // 64*wm .. +63 and weight rows 128*wn .. +127 of the tile: 2 x 4
 // v_mfma_f32_32x32x16_bf16 tiles (weights as the A operand, tokens as B),
@@ -116,9 +121,24 @@ __device__ __forceinline__ int wave_min(int v) {
   return v;
 }
 
-template <bool GATED, int kPfx>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void tiled_kernel(GemmArgs a) {
+// Two GEMMs of one kind in one launch: the tiles of sp (static rows, e.g. the
+// shared experts over every token; sp_tiles of them, 0 when absent) come
+// first, then those of g (the routed experts).  One grid keeps every CU busy
+// across both: neither leaves a partly filled last round on its own.
+struct TiledArgs {
+  GemmArgs g;
+  GemmArgs sp;
+  int sp_tiles;
+};
+
+// PAIR = false compiles the one-problem kernel: every problem selection
+// below folds to g.
+template <bool GATED, int kPfx, bool PAIR>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void tiled_kernel(TiledArgs ta) {
   using C = Stage;
+  const GemmArgs& a = ta.g;
+  const GemmArgs& sp = ta.sp;
+  const int sp_tiles = PAIR ? ta.sp_tiles : 0;
   constexpr int OUT_COLS = GATED ? kBN / 2 : kBN;
   constexpr uint32_t kInvalid = 0x80000000u;
   constexpr int kRecords = 0x7fffffff;
@@ -160,23 +180,25 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     }
     total_mt = carry;
   }
-  const int total_tiles = total_mt * n_tiles_n;
+  const int total_tiles = sp_tiles + total_mt * n_tiles_n;
   const int per_xcd = gridDim.x / 8;
   const int first = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
   if (first >= total_tiles) return;
-  const int nkb = ceil_div(a.K, C::BK);
+  const int sp_mt = sp_tiles > 0 ? ceil_div(sp.static_rows, kBM) : 1;
 
   struct TileInfo {
-    int g, row_base, m, m0, nt;
+    int p, g, row_base, m, m0, nt;  // p: 0 for sp, 1 for g
   };
   // group of tile t: the number of groups whose tiles all precede t
-  auto tile_info = [&](int t) {
+  auto tile_info = [&](int t_all) {
     TileInfo ti;
-    int mg = total_mt, base = 0;
+    ti.p = (PAIR && t_all < sp_tiles) ? 0 : 1;
+    const int t = ti.p ? t_all - sp_tiles : t_all;
+    int mg = ti.p ? total_mt : sp_mt, base = 0;
     ti.g = 0;
     ti.row_base = 0;
-    ti.m = a.static_rows;
-    if (a.offsets != nullptr) {
+    ti.m = ti.p ? a.static_rows : sp.static_rows;
+    if (ti.p && a.offsets != nullptr) {
       int cnt = 0, lo = 0, hi = 0x7fffffff;
 #pragma unroll
       for (int i = 0; i < kPfx; ++i) {
@@ -199,6 +221,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const int local = t - base;
     ti.nt = local / mg;
     ti.m0 = (local - ti.nt * mg) * kBM;
+    if (PAIR) ti.p = __builtin_amdgcn_readfirstlane(ti.p);
     ti.g = __builtin_amdgcn_readfirstlane(ti.g);
     ti.row_base = __builtin_amdgcn_readfirstlane(ti.row_base);
     ti.m = __builtin_amdgcn_readfirstlane(ti.m);
@@ -220,27 +243,33 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   __amdgpu_buffer_rsrc_t rs_x, rs_w;
   uint32_t xoff[C::LPP], woff[C::LPP];
   int x_tile = first, x_kb = 0, w_tile = first, w_kb = 0;
+  int x_p = 1, w_p = 1, x_nkb = 1, w_nkb = 1;  // each stream's problem and its K stages
   uint32_t kx0 = 0, kx1 = 0, kw0 = 0, kw1 = 0;
+  auto prob = [&](int p) -> const GemmArgs& { return (!PAIR || p) ? a : sp; };
+  const int nkb_g = ceil_div(a.K, C::BK);
 
   auto x_setup = [&](int t_in) {
     const bool live = t_in < total_tiles;
     const uint32_t dead = live ? 0u : kInvalid;
     const int t = live ? t_in : total_tiles - 1;
     const TileInfo ti = tile_info(t);
+    x_p = PAIR ? ti.p : 1;
+    const GemmArgs& q = prob(x_p);
+    x_nkb = PAIR ? ceil_div(q.K, C::BK) : nkb_g;
     const int ln = opaque_lane_id();
-    const uint16_t* xb = a.x_rows ? a.x : a.x + static_cast<size_t>(ti.row_base + ti.m0) * a.K;
+    const uint16_t* xb = q.x_rows ? q.x : q.x + static_cast<size_t>(ti.row_base + ti.m0) * q.K;
     rs_x = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(xb), 0, kRecords, kRsrcWord3);
     int xr[C::LPP];
 #pragma unroll
     for (int i = 0; i < C::LPP; ++i) {
       const int r = 32 * wave + C::RPI * i + ln / C::CPR;
       xr[i] = r;
-      if (a.x_rows) xr[i] = a.x_rows[ti.row_base + (ti.m0 + r < ti.m ? ti.m0 + r : 0)];
+      if (q.x_rows) xr[i] = q.x_rows[ti.row_base + (ti.m0 + r < ti.m ? ti.m0 + r : 0)];
     }
 #pragma unroll
     for (int i = 0; i < C::LPP; ++i) {
       const int r = 32 * wave + C::RPI * i + ln / C::CPR;
-      xoff[i] = (ti.m0 + r < ti.m ? static_cast<uint32_t>(xr[i] * a.K * 2 + chunk_of(i, ln) * 16) : kInvalid) | dead;
+      xoff[i] = (ti.m0 + r < ti.m ? static_cast<uint32_t>(xr[i] * q.K * 2 + chunk_of(i, ln) * 16) : kInvalid) | dead;
     }
   };
   auto w_setup = [&](int t_in) {
@@ -248,43 +277,48 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     const uint32_t dead = live ? 0u : kInvalid;
     const int t = live ? t_in : total_tiles - 1;
     const TileInfo ti = tile_info(t);
+    w_p = PAIR ? ti.p : 1;
+    const GemmArgs& q = prob(w_p);
+    w_nkb = PAIR ? ceil_div(q.K, C::BK) : nkb_g;
     const int ln = opaque_lane_id();
     const int col0 = ti.nt * OUT_COLS;
-    const size_t gofs = static_cast<size_t>(ti.g) * a.group_stride + static_cast<size_t>(col0) * a.ldw;
-    rs_w = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>((w_up ? a.w1 : a.w0) + gofs), 0, kRecords, kRsrcWord3);
+    const size_t gofs = static_cast<size_t>(ti.g) * q.group_stride + static_cast<size_t>(col0) * q.ldw;
+    rs_w = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>((w_up ? q.w1 : q.w0) + gofs), 0, kRecords, kRsrcWord3);
 #pragma unroll
     for (int i = 0; i < C::LPP; ++i) {
       const int r = 32 * wave + C::RPI * i + ln / C::CPR;
       const int lcol = GATED ? (r >> 7) * 64 + (r & 63) : r;
-      woff[i] = ((col0 + lcol < a.N) ? static_cast<uint32_t>(lcol * a.ldw * 2 + chunk_of(i, ln) * 16) : kInvalid) | dead;
+      woff[i] = ((col0 + lcol < q.N) ? static_cast<uint32_t>(lcol * q.ldw * 2 + chunk_of(i, ln) * 16) : kInvalid) | dead;
     }
   };
-  auto kmask = [&](int kb, int p) { return kb * C::BK + chunk_of(p, lane) * 8 < a.K ? 0u : kInvalid; };
+  auto kmask = [&](int kb, int p, int K) { return kb * C::BK + chunk_of(p, lane) * 8 < K ? 0u : kInvalid; };
   auto x_kstep = [&]() {
     const uint32_t k = static_cast<uint32_t>(x_kb * C::BK * 2);
-    kx0 = k | kmask(x_kb, 0);
-    kx1 = k | kmask(x_kb, 1);
+    const int K = prob(x_p).K;
+    kx0 = k | kmask(x_kb, 0, K);
+    kx1 = k | kmask(x_kb, 1, K);
   };
   auto w_kone = [&](int p) -> uint32_t {
+    const GemmArgs& q = prob(w_p);
     const int k0 = w_kb * C::BK;
     uint32_t w;
-    if (a.kseg >= a.K) {
+    if (q.kseg >= q.K) {
       w = static_cast<uint32_t>(k0 * 2);
-    } else if (a.kseg % C::BK == 0) {
-      const int seg = k0 / a.kseg;
-      w = static_cast<uint32_t>((static_cast<size_t>(seg) * a.seg_stride + (k0 - seg * a.kseg)) * 2);
+    } else if (q.kseg % C::BK == 0) {
+      const int seg = k0 / q.kseg;
+      w = static_cast<uint32_t>((static_cast<size_t>(seg) * q.seg_stride + (k0 - seg * q.kseg)) * 2);
     } else {
-      const int kk = min(k0 + chunk_of(p, lane) * 8, a.K - 8);
-      w = static_cast<uint32_t>((weight_col_offset(a, kk) - static_cast<size_t>(kk - k0)) * 2);
+      const int kk = min(k0 + chunk_of(p, lane) * 8, q.K - 8);
+      w = static_cast<uint32_t>((weight_col_offset(q, kk) - static_cast<size_t>(kk - k0)) * 2);
     }
-    return w | kmask(w_kb, p);
+    return w | kmask(w_kb, p, q.K);
   };
   auto w_kstep = [&]() {
     kw0 = w_kone(0);
     kw1 = w_kone(1);
   };
   auto x_advance = [&]() {
-    if (++x_kb == nkb) {
+    if (++x_kb == (PAIR ? x_nkb : nkb_g)) {
       x_kb = 0;
       x_tile += gridDim.x;
       x_setup(x_tile);
@@ -292,7 +326,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     x_kstep();
   };
   auto w_advance = [&]() {
-    if (++w_kb == nkb) {
+    if (++w_kb == (PAIR ? w_nkb : nkb_g)) {
       w_kb = 0;
       w_tile += gridDim.x;
       w_setup(w_tile);
@@ -339,6 +373,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       for (int tm = 0; tm < 2; ++tm) acc[tn][tm] = f32x16{};
   };
   auto epilogue = [&](const TileInfo& ti) {
+    const GemmArgs& pr = prob(ti.p);
     const int ln = opaque_lane_id();
     const int erow = ln & 31, ehalf = ln >> 5;
     constexpr int WCOLS = GATED ? 64 : 128;
@@ -348,11 +383,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     // drops, so the stores need no branches and the conversions of all of
     // a row group's tiles can overlap.
     const __amdgpu_buffer_rsrc_t rs_o = __builtin_amdgcn_make_buffer_rsrc(
-        a.out + static_cast<size_t>(ti.row_base + ti.m0) * a.N, 0, kRecords, kRsrcWord3);
+        pr.out + static_cast<size_t>(ti.row_base + ti.m0) * pr.N, 0, kRecords, kRsrcWord3);
 #pragma unroll
     for (int tm = 0; tm < 2; ++tm) {
       const int r = xrow0 + tm * 32 + erow;  // row within the tile
-      const uint32_t row_off = ti.m0 + r < ti.m ? static_cast<uint32_t>(r * a.N * 2) : kInvalid;
+      const uint32_t row_off = ti.m0 + r < ti.m ? static_cast<uint32_t>(r * pr.N * 2) : kInvalid;
       constexpr int TOUT = GATED ? 2 : 4;
 #pragma unroll
       for (int tn = 0; tn < TOUT; ++tn) {
@@ -379,7 +414,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
           const auto s1 = __builtin_amdgcn_permlane32_swap(pk[4 * q + 1], pk[4 * q + 3], false, false);
           const u32x4 v = {s0[0], s1[0], s0[1], s1[1]};
           const int col = col_w + tn * 32 + 16 * q + 8 * ehalf;
-          const uint32_t off = col < a.N ? row_off + static_cast<uint32_t>(col * 2) : kInvalid;
+          const uint32_t off = col < pr.N ? row_off + static_cast<uint32_t>(col * 2) : kInvalid;
           __builtin_amdgcn_raw_buffer_store_b128(v, rs_o, off | (row_off & kInvalid), 0, 0);
         }
       }
@@ -417,6 +452,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   int j = 0;
   for (int t = first; t < total_tiles; t += gridDim.x) {
     const TileInfo cur = tile_info(t);  // scalars, held through the K loop
+    const int nkb = PAIR ? ceil_div(prob(cur.p).K, C::BK) : nkb_g;
     for (int kb = 0; kb < nkb; ++kb, ++j) {
       // K-step 0 with the second half of W of stage j + 1, K-steps 1 and 2
       // with X of stage j + 2: two loads per wave and K-step
@@ -464,51 +500,54 @@ int device_cu_count() {
   return cus;
 }
 
-template <bool GATED, int PFX>
-hipError_t launch_pfx(const GemmArgs& a, long long grid, hipStream_t st) {
+template <bool GATED, int PFX, bool PAIR>
+hipError_t launch_pfx_t(const TiledArgs& ta, long long grid, hipStream_t st) {
   static unsigned long long lds_set = 0;  // devices with the LDS limit raised
   const hipError_t e_lds =
-      set_max_dynamic_lds(reinterpret_cast<const void*>(&tiled_kernel<GATED, PFX>),
+      set_max_dynamic_lds(reinterpret_cast<const void*>(&tiled_kernel<GATED, PFX, PAIR>),
                           Stage::LDS, &lds_set);
   if (e_lds != hipSuccess) return e_lds;
-  hipLaunchKernelGGL((tiled_kernel<GATED, PFX>), dim3(static_cast<unsigned>(grid)), dim3(kThreads), Stage::LDS, st, a);
+  hipLaunchKernelGGL((tiled_kernel<GATED, PFX, PAIR>), dim3(static_cast<unsigned>(grid)), dim3(kThreads), Stage::LDS,
+                     st, ta);
   return hipGetLastError();
 }
 
-template <bool GATED>
-hipError_t launch_tiled_t(const Segments& seg, const GemmArgs& a, hipStream_t st) {
-  constexpr int OUT_COLS = GATED ? kBN / 2 : kBN;
-  const long long m_tiles = (a.offsets ? static_cast<long long>(ceil_div(seg.total_rows, kBM)) + seg.groups
-                                       : ceil_div(seg.static_rows, kBM));
-  const long long tiles = m_tiles * ceil_div(a.N, OUT_COLS);
-  if (tiles == 0) return hipSuccess;
-  long long grid = std::min<long long>(tiles, device_cu_count());  // one workgroup per CU (LDS)
-  grid = ((grid + 7) / 8) * 8;
-  // group prefix values per lane: groups <= 64 * PFX
-  if (seg.groups <= kWave) return launch_pfx<GATED, 1>(a, grid, st);
-  if (seg.groups <= 4 * kWave) return launch_pfx<GATED, 4>(a, grid, st);
-  return launch_pfx<GATED, kMaxGroups / kWave>(a, grid, st);
+template <bool GATED, int PFX>
+hipError_t launch_pfx(const TiledArgs& ta, long long grid, hipStream_t st) {
+  return ta.sp_tiles > 0 ? launch_pfx_t<GATED, PFX, true>(ta, grid, st) : launch_pfx_t<GATED, PFX, false>(ta, grid, st);
 }
 
-}  // namespace
-
-hipError_t launch_tiled(const Segments& seg, const GemmArgs& a, bool gated, hipStream_t st) {
-  if (seg.groups > kMaxGroups || a.x_blocked || a.out_blocked) return hipErrorInvalidValue;
-  // 32-bit byte offsets: a tile's X rows (all of x when rows are indexed), a
-  // group's weight columns and a tile's output rows
+// Host-side checks of one problem: no blocked layouts, at most kMaxGroups
+// groups, and 32-bit byte offsets for a tile's X rows (all of x when rows
+// are indexed), a group's weight columns and a tile's output rows.
+bool tiled_ok(const Segments& seg, const GemmArgs& a) {
+  if (seg.groups > kMaxGroups || a.x_blocked || a.out_blocked) return false;
   const size_t x_span = static_cast<size_t>(a.x_rows ? a.x_row_count : kBM) * a.K * 2;
   const size_t w_span = (static_cast<size_t>(kBN) * a.ldw +
                          (a.kseg < a.K ? static_cast<size_t>((a.K - 1) / a.kseg) * a.seg_stride : 0) + a.K) * 2;
   const size_t o_span = static_cast<size_t>(kBM + 1) * a.N * 2;
-  if (x_span >= 0x80000000ull || w_span >= 0x80000000ull || o_span >= 0x80000000ull) return hipErrorInvalidValue;
-  return gated ? launch_tiled_t<true>(seg, a, st) : launch_tiled_t<false>(seg, a, st);
+  return x_span < 0x80000000ull && w_span < 0x80000000ull && o_span < 0x80000000ull;
 }
 
-bool ffn_streams_weights(const Segments& seg) { return seg.max_rows <= kSkinnyMaxRows; }
+// g over seg, after sp (static rows, sp_rows of them; 0: no second problem)
+template <bool GATED>
+hipError_t launch_tiled_t(const Segments& seg, const GemmArgs& g, const GemmArgs& sp, int sp_rows, hipStream_t st) {
+  constexpr int OUT_COLS = GATED ? kBN / 2 : kBN;
+  TiledArgs ta{g, sp, 0};
+  if (sp_rows > 0) ta.sp_tiles = ceil_div(sp_rows, kBM) * ceil_div(sp.N, OUT_COLS);
+  const long long m_tiles = (g.offsets ? static_cast<long long>(ceil_div(seg.total_rows, kBM)) + seg.groups
+                                       : ceil_div(seg.static_rows, kBM));
+  const long long tiles = m_tiles * ceil_div(g.N, OUT_COLS) + ta.sp_tiles;
+  if (tiles == 0) return hipSuccess;
+  long long grid = std::min<long long>(tiles, device_cu_count());  // one workgroup per CU (LDS)
+  grid = ((grid + 7) / 8) * 8;
+  // group prefix values per lane: groups <= 64 * PFX
+  if (seg.groups <= kWave) return launch_pfx<GATED, 1>(ta, grid, st);
+  if (seg.groups <= 4 * kWave) return launch_pfx<GATED, 4>(ta, grid, st);
+  return launch_pfx<GATED, kMaxGroups / kWave>(ta, grid, st);
+}
 
-hipError_t launch_ffn_up(const Segments& seg, const UpArgs& u, hipStream_t st) {
-  if (u.h_blocked && !ffn_streams_weights(seg)) return hipErrorInvalidValue;
-  if (u.x_rows && (seg.offsets == nullptr || u.x_row_count <= 0)) return hipErrorInvalidValue;
+GemmArgs up_gemm(const Segments& seg, const UpArgs& u) {
   GemmArgs a{};
   a.x = u.x;
   a.x_rows = u.x_rows;
@@ -526,12 +565,10 @@ hipError_t launch_ffn_up(const Segments& seg, const UpArgs& u, hipStream_t st) {
   a.ldw = u.K;
   a.seg_stride = 0;
   a.group_stride = static_cast<size_t>(u.N) * u.K;
-  if (seg.max_rows <= kSkinnyMaxRows) return launch_skinny(seg, a, true, st);
-  return launch_tiled(seg, a, true, st);
+  return a;
 }
 
-hipError_t launch_ffn_down(const Segments& seg, const DownArgs& d, hipStream_t st) {
-  if (d.h_blocked && !ffn_streams_weights(seg)) return hipErrorInvalidValue;
+GemmArgs down_gemm(const Segments& seg, const DownArgs& d) {
   GemmArgs a{};
   a.x = d.h;
   a.x_blocked = d.h_blocked;
@@ -547,8 +584,70 @@ hipError_t launch_ffn_down(const Segments& seg, const DownArgs& d, hipStream_t s
   a.ldw = d.ldw;
   a.seg_stride = d.seg_stride;
   a.group_stride = d.group_stride;
-  if (seg.max_rows <= kSkinnyMaxRows) return launch_skinny(seg, a, false, st);
-  return launch_tiled(seg, a, false, st);
+  return a;
+}
+
+bool up_ok(const Segments& seg, const UpArgs& u) {
+  if (u.h_blocked && !ffn_streams_weights(seg)) return false;
+  return !(u.x_rows && (seg.offsets == nullptr || u.x_row_count <= 0));
+}
+
+bool down_ok(const Segments& seg, const DownArgs& d) { return !(d.h_blocked && !ffn_streams_weights(seg)); }
+
+// One GEMM on its kernel, or two in one tiled launch when both take the
+// tiled kernel, the second has static rows and on its own it would leave a
+// partly filled last round of tiles: the routed tiles then fill it.  (When
+// the shared tiles fill whole rounds the one-problem kernel is faster: the
+// two-problem selections cost it about 2%.)
+hipError_t launch_gemm2(const Segments& seg, const GemmArgs& a, const Segments* sh_seg, const GemmArgs* sh,
+                        bool gated, hipStream_t st) {
+  const bool tiled = !ffn_streams_weights(seg);
+  const int out_cols = gated ? kBN / 2 : kBN;
+  const bool merge = sh != nullptr && tiled && !ffn_streams_weights(*sh_seg) && sh_seg->offsets == nullptr &&
+                     static_cast<long long>(ceil_div(sh_seg->static_rows, kBM)) * ceil_div(sh->N, out_cols) %
+                             device_cu_count() != 0;
+  if (merge) {
+    if (!tiled_ok(seg, a) || !tiled_ok(*sh_seg, *sh)) return hipErrorInvalidValue;
+    return gated ? launch_tiled_t<true>(seg, a, *sh, sh_seg->static_rows, st)
+                 : launch_tiled_t<false>(seg, a, *sh, sh_seg->static_rows, st);
+  }
+  hipError_t e = tiled ? launch_tiled(seg, a, gated, st) : launch_skinny(seg, a, gated, st);
+  if (e != hipSuccess || sh == nullptr) return e;
+  return ffn_streams_weights(*sh_seg) ? launch_skinny(*sh_seg, *sh, gated, st) : launch_tiled(*sh_seg, *sh, gated, st);
+}
+
+}  // namespace
+
+hipError_t launch_tiled(const Segments& seg, const GemmArgs& a, bool gated, hipStream_t st) {
+  if (!tiled_ok(seg, a)) return hipErrorInvalidValue;
+  const GemmArgs none{};
+  return gated ? launch_tiled_t<true>(seg, a, none, 0, st) : launch_tiled_t<false>(seg, a, none, 0, st);
+}
+
+bool ffn_streams_weights(const Segments& seg) { return seg.max_rows <= kSkinnyMaxRows; }
+
+hipError_t launch_ffn_up(const Segments& seg, const UpArgs& u, hipStream_t st) {
+  if (!up_ok(seg, u)) return hipErrorInvalidValue;
+  return launch_gemm2(seg, up_gemm(seg, u), nullptr, nullptr, true, st);
+}
+
+hipError_t launch_ffn_up2(const Segments& seg, const UpArgs& u, const Segments& sh_seg, const UpArgs& sh,
+                          hipStream_t st) {
+  if (!up_ok(seg, u) || !up_ok(sh_seg, sh)) return hipErrorInvalidValue;
+  const GemmArgs s = up_gemm(sh_seg, sh);
+  return launch_gemm2(seg, up_gemm(seg, u), &sh_seg, &s, true, st);
+}
+
+hipError_t launch_ffn_down(const Segments& seg, const DownArgs& d, hipStream_t st) {
+  if (!down_ok(seg, d)) return hipErrorInvalidValue;
+  return launch_gemm2(seg, down_gemm(seg, d), nullptr, nullptr, false, st);
+}
+
+hipError_t launch_ffn_down2(const Segments& seg, const DownArgs& d, const Segments& sh_seg, const DownArgs& sh,
+                            hipStream_t st) {
+  if (!down_ok(seg, d) || !down_ok(sh_seg, sh)) return hipErrorInvalidValue;
+  const GemmArgs s = down_gemm(sh_seg, sh);
+  return launch_gemm2(seg, down_gemm(seg, d), &sh_seg, &s, false, st);
 }
 
 }  // namespace moe

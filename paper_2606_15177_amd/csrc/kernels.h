@@ -71,6 +71,11 @@ struct UpArgs {
   bool h_blocked;
 };
 hipError_t launch_ffn_up(const Segments& seg, const UpArgs& a, hipStream_t st);
+// The same for the routed experts (seg, a) and the shared experts (sh_seg
+// with static rows, sh): one launch when both take the tiled kernel, the
+// shared tiles first.
+hipError_t launch_ffn_up2(const Segments& seg, const UpArgs& a, const Segments& sh_seg, const UpArgs& sh,
+                          hipStream_t st);
 // True when these segments take the weight-streaming kernels (decode-sized
 // groups).
 bool ffn_streams_weights(const Segments& seg);
@@ -98,6 +103,8 @@ struct DownArgs {
   bool h_blocked;
 };
 hipError_t launch_ffn_down(const Segments& seg, const DownArgs& a, hipStream_t st);
+hipError_t launch_ffn_down2(const Segments& seg, const DownArgs& a, const Segments& sh_seg, const DownArgs& sh,
+                            hipStream_t st);
 
 // ---- combine.hip -----------------------------------------------------------
 hipError_t launch_combine(int T, int k, int H, const uint16_t* y_perm, const int32_t* inv_pos,

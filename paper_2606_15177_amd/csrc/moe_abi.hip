@@ -180,27 +180,29 @@ int run_ffn(const moe_dims* d, const uint16_t* x_perm, const int32_t* x_rows, co
   const moe::Segments shared{nullptr, 1, d->T, d->T, d->T};
   hipError_t e;
 
+  // routed and shared experts: one launch per GEMM when both take the tiled
+  // kernel, else one each
   record(taps, 2 * MOE_STAGE_FFN_UP, st);
-  e = moe::launch_ffn_up(routed, moe::UpArgs{x_perm, w->w_gate, w->w_up, h, d->H, d->I, x_rows, d->T, fw.h_blocked},
-                         st);
+  const moe::UpArgs up{x_perm, w->w_gate, w->w_up, h, d->H, d->I, x_rows, d->T, fw.h_blocked};
+  if (d->n_shared > 0)
+    e = moe::launch_ffn_up2(routed, up, shared, moe::UpArgs{x, w->sh_gate, w->sh_up, h_sh, d->H, shw, nullptr, 0, false},
+                            st);
+  else
+    e = moe::launch_ffn_up(routed, up, st);
   if (e != hipSuccess) return MOE_ERR_DEVICE;
-  if (d->n_shared > 0) {
-    e = moe::launch_ffn_up(shared, moe::UpArgs{x, w->sh_gate, w->sh_up, h_sh, d->H, shw, nullptr, 0, false}, st);
-    if (e != hipSuccess) return MOE_ERR_DEVICE;
-  }
   record(taps, 2 * MOE_STAGE_FFN_UP + 1, st);
 
   record(taps, 2 * MOE_STAGE_FFN_DOWN, st);
-  moe::DownArgs dn{h, w->w_down, y_perm, d->I, d->H, d->I, d->I, 0,
-                   static_cast<size_t>(d->H) * d->I, fw.h_blocked};
-  e = moe::launch_ffn_down(routed, dn, st);
+  const moe::DownArgs dn{h, w->w_down, y_perm, d->I, d->H, d->I, d->I, 0,
+                         static_cast<size_t>(d->H) * d->I, fw.h_blocked};
+  if (d->n_shared > 0)
+    e = moe::launch_ffn_down2(routed, dn, shared,
+                              moe::DownArgs{h_sh, w->sh_down, y_shared, shw, d->H, d->I_shared, d->I_shared,
+                                            static_cast<size_t>(d->H) * d->I_shared, 0, false},
+                              st);
+  else
+    e = moe::launch_ffn_down(routed, dn, st);
   if (e != hipSuccess) return MOE_ERR_DEVICE;
-  if (d->n_shared > 0) {
-    moe::DownArgs ds{h_sh, w->sh_down, y_shared, shw, d->H, d->I_shared, d->I_shared,
-                     static_cast<size_t>(d->H) * d->I_shared, 0, false};
-    e = moe::launch_ffn_down(shared, ds, st);
-    if (e != hipSuccess) return MOE_ERR_DEVICE;
-  }
   record(taps, 2 * MOE_STAGE_FFN_DOWN + 1, st);
   return MOE_OK;
 }
