@@ -112,6 +112,15 @@ def test_ffn_tile_boundaries(moe):
     assert _run_ffn(moe, cfg, wl, idx.reshape(T, 1)) == T
 
 
+@pytest.mark.parametrize("I_sh", [1024, 960])
+def test_ffn_shared_experts_with_or_without_the_routed_launch(moe, I_sh):
+    """4096 tokens and two shared experts: 2 x 1024 shared columns make 16 x 16 = 256
+    gate/up tiles, whole rounds on 256 CUs, so the shared GEMMs keep their own launches;
+    2 x 960 make 240 tiles, which run inside the routed experts' launch."""
+    cfg, wl, idx = _case(4096, 128, 16, 2, 128, 16, 2, I_sh)
+    _run_ffn(moe, cfg, wl, idx)
+
+
 def _combine(moe, T, k, H, R, with_shared, seed):
     rng = np.random.default_rng(seed)
     y = W.f32_to_bf16_bits(rng.standard_normal((max(R, 1), H)).astype(np.float32))
