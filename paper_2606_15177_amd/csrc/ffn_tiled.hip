@@ -61,6 +61,7 @@ constexpr int kBM = 256;             // token rows per tile
 constexpr int kBN = 256;             // weight rows per tile
 constexpr int kThreads = 8 * kWave;  // eight waves, two per SIMD
 constexpr int kMaxGroups = 1024;
+constexpr int kBlockM = 8;           // m-tiles per block of a static group's tile order
 
 // One K stage and the ring of its parts.
 struct Stage {
@@ -132,8 +133,12 @@ struct TiledArgs {
 };
 
 // PAIR = false compiles the one-problem kernel: every problem selection
-// below folds to g.
-template <bool GATED, int kPfx, bool PAIR>
+// below folds to g.  SBLK (one problem of static rows only, e.g. the shared
+// experts in a launch of their own) orders its tiles in blocks of kBlockM
+// m-tiles, n-tile-major inside a block: one XCD's 32 concurrent tiles are
+// then 8 m-tiles x 4 n-tiles, instead of 32 m-tiles of one n-tile, each of
+// whose token tiles would be fetched again for every n-tile.
+template <bool GATED, int kPfx, bool PAIR, bool SBLK>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void tiled_kernel(TiledArgs ta) {
   using C = Stage;
   const GemmArgs& a = ta.g;
@@ -219,8 +224,24 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       mg = __builtin_amdgcn_readfirstlane(hi) - __builtin_amdgcn_readfirstlane(lo);
     }
     const int local = t - base;
-    ti.nt = local / mg;
-    ti.m0 = (local - ti.nt * mg) * kBM;
+    if constexpr (SBLK) {
+      const int mfull = (mg / kBlockM) * kBlockM;
+      const int full_tiles = mfull * n_tiles_n;
+      if (local < full_tiles) {
+        const int b = local / (kBlockM * n_tiles_n);
+        const int r = local - b * (kBlockM * n_tiles_n);
+        ti.nt = r / kBlockM;
+        ti.m0 = (b * kBlockM + (r - ti.nt * kBlockM)) * kBM;
+      } else {
+        const int mr = mg - mfull;
+        const int r = local - full_tiles;
+        ti.nt = r / mr;
+        ti.m0 = (mfull + (r - ti.nt * mr)) * kBM;
+      }
+    } else {
+      ti.nt = local / mg;
+      ti.m0 = (local - ti.nt * mg) * kBM;
+    }
     if (PAIR) ti.p = __builtin_amdgcn_readfirstlane(ti.p);
     ti.g = __builtin_amdgcn_readfirstlane(ti.g);
     ti.row_base = __builtin_amdgcn_readfirstlane(ti.row_base);
@@ -500,21 +521,25 @@ int device_cu_count() {
   return cus;
 }
 
-template <bool GATED, int PFX, bool PAIR>
+template <bool GATED, int PFX, bool PAIR, bool SBLK>
 hipError_t launch_pfx_t(const TiledArgs& ta, long long grid, hipStream_t st) {
   static unsigned long long lds_set = 0;  // devices with the LDS limit raised
   const hipError_t e_lds =
-      set_max_dynamic_lds(reinterpret_cast<const void*>(&tiled_kernel<GATED, PFX, PAIR>),
+      set_max_dynamic_lds(reinterpret_cast<const void*>(&tiled_kernel<GATED, PFX, PAIR, SBLK>),
                           Stage::LDS, &lds_set);
   if (e_lds != hipSuccess) return e_lds;
-  hipLaunchKernelGGL((tiled_kernel<GATED, PFX, PAIR>), dim3(static_cast<unsigned>(grid)), dim3(kThreads), Stage::LDS,
-                     st, ta);
+  hipLaunchKernelGGL((tiled_kernel<GATED, PFX, PAIR, SBLK>), dim3(static_cast<unsigned>(grid)), dim3(kThreads),
+                     Stage::LDS, st, ta);
   return hipGetLastError();
 }
 
 template <bool GATED, int PFX>
 hipError_t launch_pfx(const TiledArgs& ta, long long grid, hipStream_t st) {
-  return ta.sp_tiles > 0 ? launch_pfx_t<GATED, PFX, true>(ta, grid, st) : launch_pfx_t<GATED, PFX, false>(ta, grid, st);
+  if (ta.sp_tiles > 0) return launch_pfx_t<GATED, PFX, true, false>(ta, grid, st);
+  if constexpr (PFX == 1) {
+    if (ta.g.offsets == nullptr) return launch_pfx_t<GATED, 1, false, true>(ta, grid, st);
+  }
+  return launch_pfx_t<GATED, PFX, false, false>(ta, grid, st);
 }
 
 // Host-side checks of one problem: no blocked layouts, at most kMaxGroups
