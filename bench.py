@@ -135,14 +135,15 @@ def source_digest(names=LAYER_SOURCES) -> str:
 
 
 def measured_traffic(stage: str, workload: str):
-    """HBM bytes per launch of a stage from a committed rocprofv3 --pmc summary
-    of this workload, if it was taken on the current kernel sources (else None)."""
+    """HBM bytes of a stage per layer call (all of the stage's launches) from a
+    committed rocprofv3 --pmc summary of this workload, if it was taken on the
+    current kernel sources (else None)."""
     path = os.path.join(ROOT, "profiles", f"pmc_{workload}.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
     m_src = re.search(r"source_digest:\s*([0-9a-f]+)", text)
-    m_b = re.search(rf"hbm_bytes_per_launch_{stage}:\s*([0-9.eE+]+)", text)
+    m_b = re.search(rf"hbm_bytes_per_call_{stage}:\s*([0-9.eE+]+)", text)
     if not m_src or not m_b or m_src.group(1) != source_digest():
         return None
     return float(m_b.group(1))
