@@ -5,7 +5,8 @@
 // (expert).  For the gate/up GEMM the 256 weight rows are 128 gate rows and
 // the 128 up rows of the same output columns, so a tile yields 128 columns of
 // h = silu(gate) * up.  Tiles are numbered group-major, then by n-tile, then
-// by m-tile, so the m-tiles that share a weight tile are neighbours; each
+// by m-tile (a launch of static rows alone: in blocks of 8 m-tiles, see
+// SBLK), so the m-tiles that share a weight tile are neighbours; each
 // XCD (workgroups are dealt round-robin to the 8 XCDs) owns a contiguous run
 // of tile ids, walked t, t + gridDim, ... by its workgroups, so they run side
 // by side on one XCD and the weights cross the fabric once.  The group of a
