@@ -4,12 +4,17 @@ dispatch + SwiGLU expert FFN + combine) on MI355X.
 
     python bench.py [--steps K] [--warmup W] [--config NAME]
 
-A step is one moe_forward over one batch of the workload (default: the
-Mixtral-shaped decode step, 64 tokens, hidden 4096, 8 experts top-2,
-intermediate 14336), inputs and bf16 weights resident in HBM.  Prints one JSON
+A step is one moe_forward over one batch of the workload, inputs and bf16
+weights resident in HBM.  The default workload is the largest that one GPU
+holds: one expert-parallel rank's share of a DeepSeek-V3-shaped layer (16384
+tokens from 8 sources, hidden 7168, top-8 of 256 experts of which 32 are
+hosted here, intermediate 2048, one shared expert).  Each timed step is cold:
+a 1 GiB read before it evicts the L2s and the Infinity Cache.  Prints one JSON
 line: whole-job tokens/s, per-stage kernel times measured live with HIP
-events on the launch stream, the roofline position of the dominant kernel and
-the CPU oracle's throughput on a bounded sample of the same workload.
+events on the launch stream, the roofline position of the dominant stage (and
+the same figure from the committed kernel trace), back-to-back (warm) steps
+as a secondary figure, and the CPU oracle's throughput on a bounded sample of
+the same workload.
 
 With a placement workload (--config place_*), a step is instead one
 moe_place_experts call: the source-aware greedy expert placement of every MoE
@@ -41,7 +46,7 @@ def parse_args(argv=None):
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=3)
-    p.add_argument("--config", default="decode_mixtral")
+    p.add_argument("--config", default="ep_share_dsv3")
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="budget of the CPU-oracle baseline sample")
@@ -149,6 +154,72 @@ def measured_traffic(stage: str, workload: str):
     return float(m_b.group(1))
 
 
+# The kernels of each stage, as named in a rocprofv3 kernel trace.
+STAGE_KERNELS = {
+    "route": ("route_kernel<", "stats_kernel"),
+    "permute": ("perm_count_kernel", "perm_scan_kernel", "perm_scatter_kernel", "perm_single_kernel"),
+    "ffn_up": ("tiled_kernel<true", "skinny_kernel<true"),
+    "ffn_down": ("tiled_kernel<false", "skinny_kernel<false"),
+    "combine": ("combine_kernel",),
+}
+
+
+def _profile_rows(path: str):
+    """(source digest, [(kernel name, cells...)]) of a committed profile
+    summary, or None when it is missing or was taken on other sources."""
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_src = re.search(r"source_digest:\s*([0-9a-f]+)", text)
+    if not m_src or m_src.group(1) != source_digest():
+        return None
+    rows = []
+    for line in text.splitlines():
+        m = re.match(r"\|\s*`([^`]*)`\s*\|(.*)\|\s*$", line)
+        if m:
+            rows.append((m.group(1), [c.strip() for c in m.group(2).split("|")]))
+    return rows
+
+
+def profiled_stage_ms(stage: str, workload: str):
+    """The stage's time per layer call in the committed kernel trace of this
+    workload (the sum of its kernels' average durations; each runs once per
+    call), if the trace was taken on the current kernel sources."""
+    rows = _profile_rows(os.path.join(ROOT, "profiles", f"kernel_trace_{workload}.md"))
+    if rows is None:
+        return None
+    us = [float(c[1]) for name, c in rows if any(k in name for k in STAGE_KERNELS[stage])]
+    return sum(us) * 1e-3 if us else None
+
+
+def profiled_clock(stage: str, workload: str):
+    """Shader clock and MFMA busy fraction of the stage's kernels from the
+    committed MFMA counter summary of this workload (current sources only)."""
+    rows = _profile_rows(os.path.join(ROOT, "profiles", f"pmc_mfma_{workload}.md"))
+    if rows is None:
+        return None
+    out = []
+    for name, c in rows:
+        if any(k in name for k in STAGE_KERNELS[stage]):
+            out.append({"kernel": name.split("::")[-1].split("(")[0], "avg_us": float(c[2]),
+                        "clock_ghz": float(c[3]), "mfma_busy": round(float(c[4].rstrip("%")) / 100, 4)})
+    return out or None
+
+
+def cpu_identity() -> dict:
+    """The host CPU's model name and logical core count."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"cpu_model": model, "cpu_count": os.cpu_count()}
+
+
 class GpuMetricsWatch:
     """amd-smi clock and power samples of GPU 0, once a second, for the whole
     run.  The watcher is started as a child process before this process
@@ -178,24 +249,44 @@ class GpuMetricsWatch:
                 "socket_power_w_max": max(power) if power else None}
 
 
+def pinned_core():
+    """Pin the calling thread to one core of its allowed set (the last one)
+    and return (core, the previous set), or (None, None) where affinity
+    cannot be set."""
+    try:
+        allowed = os.sched_getaffinity(0)
+        core = max(allowed)
+        os.sched_setaffinity(0, {core})
+        return core, allowed
+    except (AttributeError, OSError):
+        return None, None
+
+
 def cpu_baseline(cfg, wl, budget_s: float) -> dict:
-    """The CPU oracle (plain C, fp64, single thread) on a bounded sample of
-    the same workload: the first n tokens, n sized to the time budget."""
+    """The CPU oracle (plain C, fp64, single thread pinned to one core) on a
+    bounded sample of the same workload: the first n tokens, n sized to the
+    time budget."""
     from oracle import oracle
     oracle.lib()
-    t0 = time.perf_counter()
-    gate = dict(gate=cfg.gate, bias=wl.get("gate_bias"), scale=cfg.routed_scale, n_group=cfg.n_group,
-                topk_group=cfg.topk_group)
-    oracle.forward_tokens(cfg.dims, [0], wl["logits"], wl["x"], wl["local_experts"], wl, **gate)
-    per_tok = max(time.perf_counter() - t0, 1e-6)
-    n = int(max(1, min(cfg.T, budget_s / per_tok)))
-    toks = list(range(n))
-    t0 = time.perf_counter()
-    oracle.forward_tokens(cfg.dims, toks, wl["logits"], wl["x"], wl["local_experts"], wl, **gate)
-    dt = time.perf_counter() - t0
+    core, allowed = pinned_core()
+    try:
+        t0 = time.perf_counter()
+        gate = dict(gate=cfg.gate, bias=wl.get("gate_bias"), scale=cfg.routed_scale, n_group=cfg.n_group,
+                    topk_group=cfg.topk_group)
+        oracle.forward_tokens(cfg.dims, [0], wl["logits"], wl["x"], wl["local_experts"], wl, **gate)
+        per_tok = max(time.perf_counter() - t0, 1e-6)
+        n = int(max(1, min(cfg.T, budget_s / per_tok)))
+        toks = list(range(n))
+        t0 = time.perf_counter()
+        oracle.forward_tokens(cfg.dims, toks, wl["logits"], wl["x"], wl["local_experts"], wl, **gate)
+        dt = time.perf_counter() - t0
+    finally:
+        if allowed is not None:
+            os.sched_setaffinity(0, allowed)
     return {"value": n / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
             "sample": f"first {n} of {cfg.T} tokens of {cfg.name}: per-token routing + "
-                      f"SwiGLU experts + combine, fp64, single thread ({dt:.1f} s)"}
+                      f"SwiGLU experts + combine, fp64, single thread ({dt:.1f} s)",
+            "pinned_core": core, **cpu_identity()}
 
 
 def bench_place(args) -> int:
@@ -373,40 +464,56 @@ def bench_layer(args, watch) -> int:
                       moe.make_taps(offsets=offsets, events=probe_ev.ev[i * n_ev:(i + 1) * n_ev]))
     torch.cuda.synchronize()
     route_no_stats = sum(probe_ev.elapsed_ms(i * n_ev, i * n_ev + 1) for i in range(n_probe)) / n_probe
-    # cold steps: a 1 GiB write before each step evicts the L2s and the
-    # Infinity Cache, so every input comes from HBM
-    flush = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
-    cold = []
-    for i in range(n_probe):
-        flush.fill_(i & 0xFF)
-        layer.forward(logits, src, x, counts, out,
-                      moe.make_taps(offsets=offsets, events=probe_ev.ev[i * n_ev:(i + 1) * n_ev]))
-        torch.cuda.synchronize()
-        cold.append(probe_ev.elapsed_ms(i * n_ev, i * n_ev + n_ev - 1))
-    del flush
-    cold.sort()
     probe_ev.close()
     dom = max(STAGES, key=lambda n: stage_ms[n])
     dom_i = STAGES.index(dom)
 
-    events = HipEvents(2 * args.steps, ev_flags)
+    # Timed steps (primary): cold.  Before each step a 1 GiB read evicts the
+    # L2s and the 256 MB Infinity Cache (a read leaves no dirty lines to be
+    # written back during the step), so every input and weight comes from
+    # HBM.  Four timing-only events per step: the step's first and last
+    # kernels, and the dominant stage.
+    flush = torch.zeros(1 << 30, dtype=torch.uint8, device="cuda")
+    flush_sum = torch.zeros((), dtype=torch.int64, device="cuda")
+    events = HipEvents(4 * args.steps, ev_flags)
     step_taps = []
     for i in range(args.steps):
         ev = [None] * n_ev
-        ev[2 * dom_i], ev[2 * dom_i + 1] = events.ev[2 * i], events.ev[2 * i + 1]
+        ev[0], ev[n_ev - 1] = events.ev[4 * i], events.ev[4 * i + 3]
+        if ev[2 * dom_i] is None:
+            ev[2 * dom_i] = events.ev[4 * i + 1]
+        if ev[2 * dom_i + 1] is None:
+            ev[2 * dom_i + 1] = events.ev[4 * i + 2]
         step_taps.append(moe.make_taps(offsets=offsets, events=ev))
+    dom_pair = (1 if dom_i != 0 else 0, 2 if 2 * dom_i + 1 != n_ev - 1 else 3)
 
-    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    print(f"[bench] timing {args.steps} cold steps", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
+        torch.sum(flush, dim=0, dtype=torch.int64, out=flush_sum)
         layer.forward(logits, src, x, counts, out, step_taps[i])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
-    # the dominant kernel's average duration over the timed steps
-    stage_ms[dom] = sum(events.elapsed_ms(2 * i, 2 * i + 1) for i in range(args.steps)) / args.steps
+    cold_wall_ms = (t1 - t0) * 1e3 / args.steps
+    cold = [events.elapsed_ms(4 * i, 4 * i + 3) for i in range(args.steps)]
+    dom_cold = [events.elapsed_ms(4 * i + dom_pair[0], 4 * i + dom_pair[1]) for i in range(args.steps)]
     events.close()
+    del flush
+    ms_per_step = sum(cold) / len(cold)
+    cold_sorted = sorted(cold)
+    # the dominant stage's average duration over the timed steps
+    stage_ms[dom] = sum(dom_cold) / len(dom_cold)
+
+    # Secondary: warm steps, back to back with no events, wall clock.
+    print(f"[bench] timing {args.steps} warm steps", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        layer.forward(logits, src, x, counts, out, plain_taps)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    warm_ms = (t1 - t0) * 1e3 / args.steps
 
     off = offsets.cpu().numpy()
     R = int(off[-1])
@@ -432,6 +539,21 @@ def bench_layer(args, watch) -> int:
                 "frac": ds["frac_hbm"]}
     roof["traffic"] = measured_traffic(dom, cfg.name)
     roof["kernel"] = dom
+    roof["ms"] = round(stage_ms[dom], 4)
+    # the same figure from the committed rocprofv3 kernel trace of this
+    # workload (sum of the stage's kernels' average durations), when it was
+    # taken on the current kernel sources
+    prof_ms = profiled_stage_ms(dom, cfg.name)
+    if prof_ms:
+        if ds["bound"] == "mfma":
+            prof_frac = ds["flops"] / (prof_ms * 1e-3) / (MFMA_BF16_PEAK_TFLOPS * 1e12)
+        else:
+            prof_frac = ds["bytes"] / (prof_ms * 1e-3) / (HBM_PEAK_GBS * 1e9)
+        roof["profile"] = {"ms": round(prof_ms, 4), "frac": round(prof_frac, 4),
+                           "source": f"profiles/kernel_trace_{cfg.name}.md"}
+    else:
+        roof["profile"] = None
+    roof["clock"] = profiled_clock(dom, cfg.name)
     ffn_ms = stage_ms["ffn_up"] + stage_ms["ffn_down"]
     ffn_flops = work["ffn_up"]["flops"] + work["ffn_down"]["flops"]
     ffn_frac_mfma = ffn_flops / (ffn_ms * 1e-3) / (MFMA_BF16_PEAK_TFLOPS * 1e12) if ffn_ms > 0 else 0.0
@@ -455,6 +577,8 @@ def bench_layer(args, watch) -> int:
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4),
+        "timing": "cold steps (1 GiB read before each); GPU time of each step from events around its first "
+                  "and last kernels; ms_per_step is their mean",
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -474,11 +598,12 @@ def bench_layer(args, watch) -> int:
                                    "permute": stages["permute"]["frac_hbm"],
                                    "combine": stages["combine"]["frac_hbm"]},
         "stages": stages,
-        "step_gpu_ms": {"median": round(probe_steps[len(probe_steps) // 2], 4), "min": round(probe_steps[0], 4),
-                        "samples": len(probe_steps)},
-        "cold": {"median_ms": round(cold[len(cold) // 2], 4), "min_ms": round(cold[0], 4),
-                 "tokens_per_s": round(cfg.T / (cold[len(cold) // 2] * 1e-3), 1),
-                 "note": "1 GiB written before each step; GPU time of the step"},
+        "cold": {"median_ms": round(cold_sorted[len(cold_sorted) // 2], 4), "min_ms": round(cold_sorted[0], 4),
+                 "max_ms": round(cold_sorted[-1], 4), "wall_ms_per_step_with_flush": round(cold_wall_ms, 4)},
+        "warm": {"ms_per_step": round(warm_ms, 4), "tokens_per_s": round(cfg.T / (warm_ms * 1e-3), 1),
+                 "note": "back-to-back steps, wall clock"},
+        "step_gpu_ms_warm_probe": {"median": round(probe_steps[len(probe_steps) // 2], 4),
+                                   "min": round(probe_steps[0], 4), "samples": len(probe_steps)},
         "stats_collection": {"route_ms_with_counts": round(stage_ms["route"], 4),
                              "route_ms_without_counts": round(route_no_stats, 4)},
         **({"gpu_metrics": watch.stop()} if watch else {}),

@@ -12,9 +12,14 @@
  *  - All array arguments are DEVICE pointers; moe_dims, moe_weights and
  *    moe_taps structs are HOST pointers read during the call only.
  *  - The caller owns every buffer.  The library never allocates, frees or
- *    synchronises and keeps no mutable global state; each call only enqueues
- *    kernels on `stream` (a hipStream_t passed as void*, NULL = the default
- *    stream) and returns.  Results are ready when the stream reaches them.
+ *    synchronises; each call only enqueues kernels on `stream` (a hipStream_t
+ *    passed as void*, NULL = the default stream) and returns.  Results are
+ *    ready when the stream reaches them.
+ *  - Process-wide state: per-device caches of fixed facts only, each written
+ *    once per device with atomic operations (so concurrent first calls are
+ *    safe): a bit per device for every kernel whose LDS limit has been
+ *    raised, and the compute-unit count of each device, which sizes the
+ *    expert GEMMs' persistent grids.
  *  - Every check below is made on the host before anything is enqueued; a
  *    call that returns an error has enqueued nothing.  MOE_ERR_DEVICE means a
  *    launch failed after earlier launches of the same call may have been
@@ -69,9 +74,15 @@ enum moe_status {
  *   I_shared  intermediate size of each shared expert (ignored if n_shared=0).
  *   flags     the router's gate function, a moe_gate value (its parameters
  *             travel in moe_gating).
- * Kernel limits (MOE_ERR_UNSUPPORTED beyond them): E <= 1024, k <= 32,
- * H, I, I_shared multiples of 8, I_shared a multiple of 64 when n_shared > 1,
- * T*k < 2^31.
+ * Kernel limits (MOE_ERR_UNSUPPORTED beyond them, decided on the host by
+ * moe_validate and by every entry point before it enqueues anything):
+ * E <= 1024, k <= 32, H, I, I_shared multiples of 8, T*k < 2^31, and the
+ * 32-bit byte offsets of the expert GEMMs: within one expert's weight
+ * matrices (about N*K*2 bytes), within a 256-row tile of activations or
+ * outputs (257*max(H, I, n_shared*I_shared)*2 bytes), and, in moe_forward,
+ * whose gate/up GEMM reads token rows through the dispatch list, within x
+ * (T*H*2 < 2^31, i.e. T < 149,797 at H = 7168; moe_expert_ffn reads its
+ * gathered rows tile by tile and has no such bound).
  */
 typedef struct moe_dims {
     int32_t T, H, E, k, I, S, E_local, n_shared, I_shared, flags;
@@ -165,16 +176,17 @@ const char *moe_strerror(int status);
 
 /*
  * Bytes of workspace `entry` needs for these sizes (0 when the dimensions are
- * invalid; moe_validate says why).  Host only, no HIP call.  The workspace is
+ * invalid or beyond that entry point's limits; moe_validate says why).  Host only, no HIP call.  The workspace is
  * device memory owned by the caller, at least 256-byte aligned; its contents
  * need no initialisation and are undefined after the call.
  */
 size_t moe_workspace_bytes(const moe_dims *dims, int entry);
 
 /*
- * Host-only check of dims (and, when entry != 0, of ws_bytes against
- * moe_workspace_bytes(dims, entry)).  Returns MOE_OK or the status the entry
- * points would return for these sizes.  Makes no HIP call.
+ * Host-only check of dims against the limits of entry point `entry` (0: of
+ * every entry point) and, when entry != 0, of ws_bytes against
+ * moe_workspace_bytes(dims, entry).  Returns MOE_OK or the status the entry
+ * point would return for these sizes.  Makes no HIP call.
  */
 int moe_validate(const moe_dims *dims, int entry, size_t ws_bytes);
 

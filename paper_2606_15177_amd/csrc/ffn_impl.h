@@ -45,6 +45,10 @@ __device__ __forceinline__ size_t weight_col_offset(const GemmArgs& a, int c) {
 }
 
 hipError_t launch_skinny(const Segments& seg, const GemmArgs& a, bool gated, hipStream_t st);
+// Host-side size limits of the weight-streaming kernel (launch_skinny
+// refuses arguments that fail this check; it also requires device offsets
+// for the blocked layouts).
+bool skinny_ok(const GemmArgs& a);
 constexpr int kChunkRows = kChunkRowsHost;
 constexpr int kBlockElems = 512;  // one 1 KB block of the chunk-blocked layout
 hipError_t launch_tiled(const Segments& seg, const GemmArgs& a, bool gated, hipStream_t st);

@@ -257,13 +257,18 @@ size_t chunk_capacity(int groups, int total_rows) {
   return static_cast<size_t>(total_rows / kChunkRows) + static_cast<size_t>(std::min(groups, total_rows));
 }
 
-hipError_t launch_skinny(const Segments& seg, const GemmArgs& a, bool gated, hipStream_t st) {
-  if ((a.x_blocked || a.out_blocked) && (a.offsets == nullptr || a.K % 16 != 0 || (a.out_blocked && a.N % 16 != 0)))
-    return hipErrorInvalidValue;
+bool skinny_ok(const GemmArgs& a) {
+  if ((a.x_blocked || a.out_blocked) && (a.K % 16 != 0 || (a.out_blocked && a.N % 16 != 0))) return false;
   // weight byte offsets within a group are 32-bit
   const size_t w_span = (static_cast<size_t>(a.N) * a.ldw +
                          (a.kseg < a.K ? static_cast<size_t>((a.K - 1) / a.kseg) * a.seg_stride : 0) + a.K) * 2;
-  if (w_span >= kInvalidOff) return hipErrorInvalidValue;
+  return w_span < kInvalidOff;
+}
+
+hipError_t launch_skinny(const Segments& seg, const GemmArgs& a, bool gated, hipStream_t st) {
+  // the blocked layouts are defined by the device-side offsets
+  if ((a.x_blocked || a.out_blocked) && a.offsets == nullptr) return hipErrorInvalidValue;
+  if (!skinny_ok(a)) return hipErrorInvalidValue;
   // gate/up: the gate and up blocks of 32 rows per wave; down: two 32-row
   // blocks per wave; 4 K parts, 64-wide steps, two-step rings (64 KB of LDS,
   // two workgroups per CU): the measured best shapes for the decode workload

@@ -509,17 +509,21 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   __builtin_amdgcn_s_waitcnt(kWaitAll);
 }
 
+// Compute units of the current device, looked up once per device: a
+// per-device cache of a fixed property (atomic, so concurrent callers are
+// safe), sized for the devices one process can see.
+constexpr int kMaxDevices = 64;
 int device_cu_count() {
-  static int cus = 0;
-  if (cus == 0) {
-    int dev = 0, n = 0;
-    if (hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0)
-      cus = n;
-    else
-      cus = 256;
+  static int cus[kMaxDevices] = {};
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  if (dev >= 0 && dev < kMaxDevices) {
+    const int c = __atomic_load_n(&cus[dev], __ATOMIC_RELAXED);
+    if (c > 0) return c;
   }
-  return cus;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return 256;
+  if (dev >= 0 && dev < kMaxDevices) __atomic_store_n(&cus[dev], n, __ATOMIC_RELAXED);
+  return n;
 }
 
 template <bool GATED, int PFX, bool PAIR, bool SBLK>
@@ -544,11 +548,12 @@ hipError_t launch_pfx(const TiledArgs& ta, long long grid, hipStream_t st) {
 }
 
 // Host-side checks of one problem: no blocked layouts, at most kMaxGroups
-// groups, and 32-bit byte offsets for a tile's X rows (all of x when rows
-// are indexed), a group's weight columns and a tile's output rows.
+// groups, and 32-bit byte offsets for a tile's X rows (all x_row_count rows
+// of x when rows are indexed), a group's weight columns and a tile's output
+// rows.
 bool tiled_ok(const Segments& seg, const GemmArgs& a) {
   if (seg.groups > kMaxGroups || a.x_blocked || a.out_blocked) return false;
-  const size_t x_span = static_cast<size_t>(a.x_rows ? a.x_row_count : kBM) * a.K * 2;
+  const size_t x_span = static_cast<size_t>(a.x_row_count > 0 ? a.x_row_count : kBM) * a.K * 2;
   const size_t w_span = (static_cast<size_t>(kBN) * a.ldw +
                          (a.kseg < a.K ? static_cast<size_t>((a.K - 1) / a.kseg) * a.seg_stride : 0) + a.K) * 2;
   const size_t o_span = static_cast<size_t>(kBM + 1) * a.N * 2;
@@ -620,6 +625,13 @@ bool up_ok(const Segments& seg, const UpArgs& u) {
 
 bool down_ok(const Segments& seg, const DownArgs& d) { return !(d.h_blocked && !ffn_streams_weights(seg)); }
 
+// The limits of the kernel a problem runs on (weight streaming or tiled).
+// Whether one launch takes two problems or each its own, each problem must
+// pass this, and passing it is all the launchers ask.
+bool gemm_ok(const Segments& seg, const GemmArgs& a) {
+  return ffn_streams_weights(seg) ? skinny_ok(a) : tiled_ok(seg, a);
+}
+
 // One GEMM on its kernel, or two in one tiled launch when both take the
 // tiled kernel, the second has static rows and on its own it would leave a
 // partly filled last round of tiles: the routed tiles then fill it.  (When
@@ -651,6 +663,12 @@ hipError_t launch_tiled(const Segments& seg, const GemmArgs& a, bool gated, hipS
 }
 
 bool ffn_streams_weights(const Segments& seg) { return seg.max_rows <= kSkinnyMaxRows; }
+
+bool ffn_up_supported(const Segments& seg, const UpArgs& u) { return up_ok(seg, u) && gemm_ok(seg, up_gemm(seg, u)); }
+
+bool ffn_down_supported(const Segments& seg, const DownArgs& d) {
+  return down_ok(seg, d) && gemm_ok(seg, down_gemm(seg, d));
+}
 
 hipError_t launch_ffn_up(const Segments& seg, const UpArgs& u, hipStream_t st) {
   if (!up_ok(seg, u)) return hipErrorInvalidValue;

@@ -58,7 +58,7 @@ struct Segments {
 // h[r][i] = silu(sum_c X[r][c] Wg[g][i][c]) * (sum_c X[r][c] Wu[g][i][c]),
 // weights [groups][N][K] (group stride N*K), x row stride K, h row stride N.
 // X[r] = x[r], or x[x_rows[r]] when x_rows != nullptr (the dispatch gather
-// read in place; x then has x_row_count rows).
+// read in place; x then has x_row_count rows; x_row_count is 0 otherwise).
 struct UpArgs {
   const uint16_t* x;
   const uint16_t* w_gate;
@@ -71,6 +71,10 @@ struct UpArgs {
   bool h_blocked;
 };
 hipError_t launch_ffn_up(const Segments& seg, const UpArgs& a, hipStream_t st);
+// Host only, no HIP call: whether launch_ffn_up accepts these sizes (the
+// pointers are not looked at; x_row_count > 0 stands for rows read through
+// x_rows).  launch_ffn_up2 accepts two problems when each passes.
+bool ffn_up_supported(const Segments& seg, const UpArgs& a);
 // The same for the routed experts (seg, a) and the shared experts (sh_seg
 // with static rows, sh): one launch when both take the tiled kernel, the
 // shared tiles first.
@@ -103,6 +107,8 @@ struct DownArgs {
   bool h_blocked;
 };
 hipError_t launch_ffn_down(const Segments& seg, const DownArgs& a, hipStream_t st);
+// Host only: whether launch_ffn_down accepts these sizes (as above).
+bool ffn_down_supported(const Segments& seg, const DownArgs& a);
 hipError_t launch_ffn_down2(const Segments& seg, const DownArgs& a, const Segments& sh_seg, const DownArgs& sh,
                             hipStream_t st);
 

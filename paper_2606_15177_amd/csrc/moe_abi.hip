@@ -168,40 +168,77 @@ int weights_ok(const moe_dims* d, const moe_weights* w) {
   return MOE_OK;
 }
 
-// The two grouped GEMMs of the experts (routed, then shared) + their events.
+// The two grouped GEMMs of the experts (routed, then shared): their row
+// segments and arguments, built the same way for the host-side limit check
+// (null pointers; rows_indexed says whether the gate/up GEMM reads its rows
+// through a row list of T entries) and for the launches.
+struct FfnPlan {
+  moe::Segments routed, shared;
+  moe::UpArgs up, sh_up;
+  moe::DownArgs dn, sh_dn;
+};
+FfnPlan plan_ffn(const moe_dims* d, const uint16_t* x_perm, const int32_t* x_rows, bool rows_indexed,
+                 const int32_t* offsets, const moe_weights* w, const uint16_t* x, uint16_t* y_perm,
+                 uint16_t* y_shared, void* ws) {
+  const FfnWs fw = carve_ffn(d, ws);
+  const int shw = static_cast<int>(sh_width(d));
+  FfnPlan p{};
+  p.routed = moe::Segments{offsets, d->E_local, 0, d->T, d->T * d->k};
+  p.shared = moe::Segments{nullptr, 1, d->T, d->T, d->T};
+  p.up = moe::UpArgs{x_perm, w ? w->w_gate : nullptr, w ? w->w_up : nullptr, fw.h, d->H, d->I, x_rows,
+                     rows_indexed ? d->T : 0, fw.h_blocked};
+  p.sh_up = moe::UpArgs{x, w ? w->sh_gate : nullptr, w ? w->sh_up : nullptr, fw.h_sh, d->H, shw, nullptr, 0, false};
+  p.dn = moe::DownArgs{fw.h, w ? w->w_down : nullptr, y_perm, d->I, d->H, d->I, d->I, 0,
+                       static_cast<size_t>(d->H) * d->I, fw.h_blocked};
+  p.sh_dn = moe::DownArgs{fw.h_sh, w ? w->sh_down : nullptr, y_shared, shw, d->H, d->I_shared, d->I_shared,
+                          static_cast<size_t>(d->H) * d->I_shared, 0, false};
+  return p;
+}
+
+// Kernel limits of the expert GEMMs for these sizes (MOE_ERR_UNSUPPORTED
+// beyond them), decided before anything is enqueued: the same predicates the
+// launchers apply, on the same arguments.
+int check_ffn_limits(const moe_dims* d, bool rows_indexed) {
+  if (d->T == 0) return MOE_OK;
+  const FfnPlan p = plan_ffn(d, nullptr, nullptr, rows_indexed, nullptr, nullptr, nullptr, nullptr, nullptr,
+                             nullptr);
+  if (!moe::ffn_up_supported(p.routed, p.up) || !moe::ffn_down_supported(p.routed, p.dn))
+    return MOE_ERR_UNSUPPORTED;
+  if (d->n_shared > 0 &&
+      (!moe::ffn_up_supported(p.shared, p.sh_up) || !moe::ffn_down_supported(p.shared, p.sh_dn)))
+    return MOE_ERR_UNSUPPORTED;
+  return MOE_OK;
+}
+
+// The limits of one entry point (0: of every entry point).
+int check_entry(const moe_dims* d, int entry) {
+  int s = MOE_OK;
+  if (entry == 0 || entry == MOE_ENTRY_EXPERT_FFN) s = check_ffn_limits(d, false);
+  if (s == MOE_OK && (entry == 0 || entry == MOE_ENTRY_FORWARD)) s = check_ffn_limits(d, true);
+  return s;
+}
+
 int run_ffn(const moe_dims* d, const uint16_t* x_perm, const int32_t* x_rows, const int32_t* offsets,
             const moe_weights* w, const uint16_t* x, uint16_t* y_perm, uint16_t* y_shared,
             void* ws, const moe_taps* taps, hipStream_t st) {
-  const FfnWs fw = carve_ffn(d, ws);
-  uint16_t* h = fw.h;
-  uint16_t* h_sh = fw.h_sh;
-  const int shw = static_cast<int>(sh_width(d));
-  const moe::Segments routed{offsets, d->E_local, 0, d->T, d->T * d->k};
-  const moe::Segments shared{nullptr, 1, d->T, d->T, d->T};
+  const FfnPlan p = plan_ffn(d, x_perm, x_rows, x_rows != nullptr, offsets, w, x, y_perm, y_shared, ws);
   hipError_t e;
 
   // routed and shared experts: one launch per GEMM when both take the tiled
   // kernel, else one each
   record(taps, 2 * MOE_STAGE_FFN_UP, st);
-  const moe::UpArgs up{x_perm, w->w_gate, w->w_up, h, d->H, d->I, x_rows, d->T, fw.h_blocked};
   if (d->n_shared > 0)
-    e = moe::launch_ffn_up2(routed, up, shared, moe::UpArgs{x, w->sh_gate, w->sh_up, h_sh, d->H, shw, nullptr, 0, false},
-                            st);
+    e = moe::launch_ffn_up2(p.routed, p.up, p.shared, p.sh_up, st);
   else
-    e = moe::launch_ffn_up(routed, up, st);
+    e = moe::launch_ffn_up(p.routed, p.up, st);
   if (e != hipSuccess) return MOE_ERR_DEVICE;
   record(taps, 2 * MOE_STAGE_FFN_UP + 1, st);
 
   record(taps, 2 * MOE_STAGE_FFN_DOWN, st);
-  const moe::DownArgs dn{h, w->w_down, y_perm, d->I, d->H, d->I, d->I, 0,
-                         static_cast<size_t>(d->H) * d->I, fw.h_blocked};
   if (d->n_shared > 0)
-    e = moe::launch_ffn_down2(routed, dn, shared,
-                              moe::DownArgs{h_sh, w->sh_down, y_shared, shw, d->H, d->I_shared, d->I_shared,
-                                            static_cast<size_t>(d->H) * d->I_shared, 0, false},
-                              st);
+    e = moe::launch_ffn_down2(p.routed, p.dn, p.shared, p.sh_dn, st);
   else
-    e = moe::launch_ffn_down(routed, dn, st);
+    e = moe::launch_ffn_down(p.routed, p.dn, st);
   if (e != hipSuccess) return MOE_ERR_DEVICE;
   record(taps, 2 * MOE_STAGE_FFN_DOWN + 1, st);
   return MOE_OK;
@@ -227,12 +264,14 @@ const char* moe_strerror(int s) {
 }
 
 size_t moe_workspace_bytes(const moe_dims* d, int entry) {
-  if (check_dims(d) != MOE_OK) return 0;
+  if (check_dims(d) != MOE_OK || check_entry(d, entry) != MOE_OK) return 0;
   return entry_ws(d, entry);
 }
 
 int moe_validate(const moe_dims* d, int entry, size_t ws_bytes) {
   int s = check_dims(d);
+  if (s != MOE_OK) return s;
+  s = check_entry(d, entry);
   if (s != MOE_OK) return s;
   if (entry != 0 && ws_bytes < entry_ws(d, entry)) return MOE_ERR_WORKSPACE;
   return MOE_OK;
@@ -295,6 +334,8 @@ int moe_expert_ffn(const moe_dims* d, const moe_bf16* x_perm, const int32_t* off
   if (d->n_shared > 0 && (!x || !y_shared)) return MOE_ERR_NULL;
   if (!aligned16(x_perm) || !aligned16(y_perm)) return MOE_ERR_ALIGN;
   if (d->n_shared > 0 && (!aligned16(x) || !aligned16(y_shared))) return MOE_ERR_ALIGN;
+  s = check_entry(d, MOE_ENTRY_EXPERT_FFN);
+  if (s != MOE_OK) return s;
   s = check_ws(d, MOE_ENTRY_EXPERT_FFN, ws, ws_bytes);
   if (s != MOE_OK) return s;
   if (d->T == 0) return MOE_OK;
@@ -327,6 +368,8 @@ int moe_forward(const moe_dims* d, const moe_gating* gating, const float* logits
   if (d->T > 0 && (!logits || !x || !out)) return MOE_ERR_NULL;
   if (counts && d->T > 0 && !src) return MOE_ERR_NULL;
   if (d->T > 0 && (!aligned16(x) || !aligned16(out))) return MOE_ERR_ALIGN;
+  s = check_entry(d, MOE_ENTRY_FORWARD);
+  if (s != MOE_OK) return s;
   s = check_ws(d, MOE_ENTRY_FORWARD, ws, ws_bytes);
   if (s != MOE_OK) return s;
 

@@ -3,7 +3,9 @@ cached workloads.  Inputs come from the seeded generator only; expected
 values come from the CPU oracle only."""
 from __future__ import annotations
 
+import concurrent.futures as cf
 import functools
+import os
 
 import numpy as np
 import torch
@@ -104,3 +106,21 @@ def gating_cfg(moe, cfg, wl, keep=None):
     b = wl.get("gate_bias")
     bias = None if b is None else dev(b)
     return moe.gating(bias, cfg.routed_scale, cfg.n_group, cfg.topk_group), bias
+
+
+def host_threads() -> int:
+    """Worker threads for the oracle: the CPUs this process may use, at most 16."""
+    return max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+def parallel_rows(fn, items):
+    """fn(items[a:b]) over disjoint slices in host threads, results stacked in
+    order.  The C oracle is reentrant and ctypes releases the interpreter lock
+    during the call, so the slices run in parallel."""
+    items = np.asarray(items)
+    if len(items) == 0:
+        return fn(items)
+    parts = np.array_split(items, min(host_threads(), len(items)))
+    with cf.ThreadPoolExecutor(len(parts)) as ex:
+        res = list(ex.map(fn, parts))
+    return np.concatenate(res, axis=0)

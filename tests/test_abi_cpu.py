@@ -204,3 +204,46 @@ def test_gating_rejects_before_launch(moe, flags, g, code):
         d = moe.dims(T=4, H=64, E=256, k=4, I=64, S=2, E_local=256, flags=flags)
     gat = moe.MoeGating(g.get("bias"), g.get("routed_scale", 1.0), n_group, g.get("topk_group", 0))
     assert moe._lib.moe_route(C.byref(d), C.byref(gat), None, None, None, None) == code
+
+
+# ------------------------------------------------------- kernel limits ----
+
+def test_kernel_limits_decided_on_the_host(moe):
+    """The tiled gate/up GEMM of moe_forward reads token rows through the
+    dispatch list with 32-bit byte offsets from the start of x, so T*H*2 must
+    stay below 2^31 (T >= 149,797 at H = 7168 does not).  moe_validate and
+    moe_forward say so before anything is enqueued; moe_expert_ffn, which
+    reads a gathered copy tile by tile, takes the same sizes."""
+    import numpy as np
+    lib = moe._lib
+    big = moe.dims(T=150000, H=7168, E=256, k=8, I=2048, S=8, E_local=32, n_shared=1, I_shared=2048)
+    assert moe.validate(big, moe.ENTRY_FORWARD) == moe.MOE_ERR_UNSUPPORTED
+    assert moe.validate(big) == moe.MOE_ERR_UNSUPPORTED                  # entry 0: every entry point
+    assert moe.workspace_bytes(big, moe.ENTRY_FORWARD) == 0
+    assert moe.validate(big, moe.ENTRY_EXPERT_FFN, 1 << 62) == moe.MOE_OK
+    assert moe.validate(big, moe.ENTRY_PERMUTE, 1 << 62) == moe.MOE_OK
+    ok = moe.dims(T=149000, H=7168, E=256, k=8, I=2048, S=8, E_local=32, n_shared=1, I_shared=2048)
+    assert moe.validate(ok, moe.ENTRY_FORWARD, 1 << 62) == moe.MOE_OK
+    # moe_forward returns the same code with nothing launched: host buffers
+    # stand in for every device pointer (nothing may touch them) and the
+    # counts matrix stays as it was
+    counts = np.arange(8 * 256, dtype=np.int64)
+    before = counts.copy()
+    buf = np.zeros(1 << 12, dtype=np.uint8)
+    p = buf.ctypes.data + (-buf.ctypes.data) % 256
+    w = moe.MoeWeights(p, p, p, p, p, p)
+    rc = lib.moe_forward(C.byref(big), None, p, p, p, p, C.byref(w), counts.ctypes.data, p, None, p,
+                         1 << 62, None)
+    assert rc == moe.MOE_ERR_UNSUPPORTED
+    assert np.array_equal(counts, before)
+
+
+@pytest.mark.parametrize("change", [
+    dict(T=1024, H=8, E=8, k=2, I=2 ** 22, E_local=8),               # a tiled tile's output rows: 257*I*2 >= 2^31
+    dict(T=16, H=2 ** 16, E=8, k=2, I=2 ** 15, E_local=8),           # streamed weights of one expert: I*H*2 >= 2^31
+])
+def test_kernel_limits_of_each_gemm(moe, change):
+    d = moe.dims(S=2, **change)
+    assert moe.validate(d, moe.ENTRY_EXPERT_FFN, 1 << 62) == moe.MOE_ERR_UNSUPPORTED
+    assert moe.validate(d, moe.ENTRY_FORWARD, 1 << 62) == moe.MOE_ERR_UNSUPPORTED
+    assert moe.validate(d, moe.ENTRY_PERMUTE, 1 << 62) == moe.MOE_OK

@@ -7,7 +7,7 @@ import torch
 
 from oracle import oracle
 from paper_2606_15177_amd import workloads as W
-from tests.gpu_util import assert_layer_close, bf16_f64, dev, dev_weights, host_bf16
+from tests.gpu_util import assert_layer_close, bf16_f64, dev, dev_weights, host_bf16, parallel_rows
 
 pytestmark = pytest.mark.gpu
 
@@ -47,15 +47,18 @@ def _run_ffn(moe, cfg, wl, idx):
                    y_perm, ysh, ws)
     torch.cuda.synchronize()
     slots = np.repeat(np.arange(cfg.E_local), np.diff(off)).astype(np.int32)
-    ref = oracle.ffn_rows(xp, slots, wl["w_gate"], wl["w_up"], wl["w_down"])
-    got = host_bf16(y_perm)[:R]
     if R:
-        assert_layer_close(got, ref, "y_perm")
+        ref = parallel_rows(lambda p: oracle.ffn_rows(xp[p], slots[p], wl["w_gate"], wl["w_up"], wl["w_down"]),
+                            np.arange(R))
+        assert_layer_close(host_bf16(y_perm)[:R], ref, "y_perm")
     if cfg.n_shared:
-        ref_sh = np.zeros((cfg.T, cfg.H))
-        for t in range(cfg.T):
-            for q in range(cfg.n_shared):
-                ref_sh[t] += oracle.swiglu_ffn(wl["x"][t], wl["sh_gate"][q], wl["sh_up"][q], wl["sh_down"][q])
+        def shared_rows(part):
+            y = np.zeros((len(part), cfg.H))
+            for i, t in enumerate(part):
+                for q in range(cfg.n_shared):
+                    y[i] += oracle.swiglu_ffn(wl["x"][t], wl["sh_gate"][q], wl["sh_up"][q], wl["sh_down"][q])
+            return y
+        ref_sh = parallel_rows(shared_rows, np.arange(cfg.T))
         assert_layer_close(host_bf16(ysh), ref_sh, "y_shared")
     return R
 
@@ -118,6 +121,23 @@ def test_ffn_shared_experts_with_or_without_the_routed_launch(moe, I_sh):
     gate/up tiles, whole rounds on 256 CUs, so the shared GEMMs keep their own launches;
     2 x 960 make 240 tiles, which run inside the routed experts' launch."""
     cfg, wl, idx = _case(4096, 128, 16, 2, 128, 16, 2, I_sh)
+    _run_ffn(moe, cfg, wl, idx)
+
+
+@pytest.mark.parametrize("T,H,I_sh,which", [
+    (1000, 128, 8192, "up"),       # 4 m-tiles x 64 column tiles: all tiles past the last whole block
+    (2900, 128, 8192, "up"),       # 12 m-tiles: one whole block of 8, then the remainder of 4
+    (1000, 16376, 64, "down"),     # the down projection's 64 column tiles (H = 16376)
+    (2900, 16376, 64, "down"),
+])
+def test_ffn_shared_blocked_order_remainder(moe, T, H, I_sh, which):
+    """A launch of the shared experts alone (their tiles fill whole rounds of
+    the 256 compute units) orders its tiles in blocks of 8 m-tiles; these
+    shapes have m-tile counts that are not multiples of 8, so the tiles past
+    the last whole block take the remainder order.  Every row is checked."""
+    if torch.cuda.get_device_properties(0).multi_processor_count != 256:
+        pytest.skip("the shapes fill whole rounds of 256 compute units")
+    cfg, wl, idx = _case(T, H, 8, 2, 64, 8, 1, I_sh)
     _run_ffn(moe, cfg, wl, idx)
 
 

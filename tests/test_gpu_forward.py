@@ -1,8 +1,8 @@
-"""Whole-layer GPU parity (moe_forward) against the CPU oracle: every
-intermediate the layer exposes bit-exact (expert ids, counts, offsets,
-dispatch order), gates within 1e-6 and the output within the layer
-tolerance; at the five workloads' full sizes the output is checked on sampled
-tokens, each computed by the oracle from the definition."""
+"""Whole-layer GPU parity (moe_forward) against the CPU oracle on small and
+adversarial layers: every intermediate the layer exposes bit-exact (expert
+ids, counts, offsets, dispatch order), gates within 1e-6 and the output
+within the layer tolerance.  The five workloads at full size are in
+test_gpu_full_size.py."""
 import numpy as np
 import pytest
 import torch
@@ -10,7 +10,7 @@ import torch
 from oracle import oracle
 from paper_2606_15177_amd import workloads as W
 from tests.gpu_util import (assert_gates_close, assert_layer_close, dev, dev_weights, gating_cfg, host_bf16,
-                            oracle_forward_cfg, oracle_route_cfg, sample_tokens, workload)
+                            oracle_forward_cfg, oracle_route_cfg, workload)
 
 pytestmark = pytest.mark.gpu
 
@@ -128,26 +128,6 @@ def test_forward_empty_batch(moe):
     assert counts.sum().item() == 0
 
 
-@pytest.mark.slow
-@pytest.mark.parametrize("name", W.CONFIG_ORDER)
-def test_forward_full_size(moe, name):
-    """Every routing intermediate over all tokens, and the output on sampled
-    tokens, at the workload's full size and in the bench's launch configuration."""
-    cfg = W.CONFIGS[name]
-    wl = workload(name)
-    res = _forward(moe, cfg, wl)
-    ridx = _check_routing(cfg, wl, res)
-    n = {"decode_mixtral": 12, "ep_share_dsv3": 12}.get(name, 24)
-    extra = []
-    if wl["local_experts"] is not None:    # include tokens that have no local expert
-        local = set(wl["local_experts"].tolist())
-        extra = [t for t in range(cfg.T) if not (set(ridx[t].tolist()) & local)][:2]
-    toks = sample_tokens(cfg.T, n, seed=1, extra=extra)
-    ref = oracle.forward_tokens(cfg.dims, toks, wl["logits"], wl["x"], wl["local_experts"], wl)
-    e = assert_layer_close(res["outs"][0][toks], ref, name)
-    print(f"{name}: rel {e['rel']:.2e} mae {e['mae']:.2e} rel_mae {e['rel_mae']:.2e}")
-
-
 @pytest.mark.parametrize("variant", [
     dict(gate=1),
     dict(gate=1, n_group=4, topk_group=2, routed_scale=2.0),
@@ -164,16 +144,3 @@ def test_forward_gated_routers(moe, variant):
     _check_routing(cfg, wl, res)
     ref = oracle_forward_cfg(cfg, wl, np.arange(cfg.T))
     assert_layer_close(res["outs"][0], ref, str(variant))
-
-
-@pytest.mark.slow
-def test_forward_v3_router_full_size_sampled(moe):
-    """The DeepSeek-V3 share with DeepSeek-V3's router at full size: routing
-    and dispatch bit-exact, sampled tokens of the output against the oracle."""
-    cfg = W.CONFIGS["ep_share_dsv3_v3router"]
-    wl = workload(cfg.name)
-    res = _forward(moe, cfg, wl)
-    _check_routing(cfg, wl, res)
-    toks = sample_tokens(cfg.T, 12, seed=1)
-    ref = oracle_forward_cfg(cfg, wl, toks)
-    assert_layer_close(res["outs"][0][toks], ref, cfg.name)
