@@ -15,11 +15,13 @@
  *    synchronises; each call only enqueues kernels on `stream` (a hipStream_t
  *    passed as void*, NULL = the default stream) and returns.  Results are
  *    ready when the stream reaches them.
- *  - Process-wide state: per-device caches of fixed facts only, each written
+ *  - Process-wide state: per-device caches of fixed facts, each written
  *    once per device with atomic operations (so concurrent first calls are
  *    safe): a bit per device for every kernel whose LDS limit has been
- *    raised, and the compute-unit count of each device, which sizes the
- *    expert GEMMs' persistent grids.
+ *    raised, the compute-unit count of each device, which sizes the expert
+ *    GEMMs' persistent grids, and the address of each device's copy of
+ *    moe_forward_noalloc's scratch array.  That array is the only mutable
+ *    device state the library owns; only moe_forward_noalloc uses it.
  *  - Every check below is made on the host before anything is enqueued; a
  *    call that returns an error has enqueued nothing.  MOE_ERR_DEVICE means a
  *    launch failed after earlier launches of the same call may have been
@@ -301,6 +303,33 @@ int moe_forward(const moe_dims *dims, const moe_gating *gating,
                 const moe_bf16 *x, const int32_t *local_experts,
                 const moe_weights *weights, int64_t *counts, moe_bf16 *out,
                 const moe_taps *taps, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * moe_forward without a caller workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, hosts
+ * that forbid allocation): the forward workspace lives in a library-owned
+ * device array of MOE_NOALLOC_SCRATCH_BYTES (32 MiB), one copy per device,
+ * held by every device the library runs on until the process ends.  The
+ * call allocates and frees nothing; the caller still passes every input and
+ * output.  Arguments and results are those of moe_forward.
+ *   - Sizes whose forward workspace (moe_workspace_bytes(dims,
+ *     MOE_ENTRY_FORWARD)) exceeds MOE_NOALLOC_SCRATCH_BYTES return
+ *     MOE_ERR_WORKSPACE before anything is enqueued: decode-sized batches
+ *     fit (64 tokens of a hidden-4096, intermediate-14336, top-2 layer need
+ *     about 12 MB).
+ *   - `stream` must belong to the current device (else MOE_ERR_DEVICE); the
+ *     current device's copy of the array is used.
+ *   - Every call on a device shares that device's array, which keeps the
+ *     last call's contents: calls that overlap on one device, on any
+ *     streams, race and must be serialised by the caller.
+ */
+#define MOE_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+
+int moe_forward_noalloc(const moe_dims *dims, const moe_gating *gating,
+                        const float *logits, const int32_t *src,
+                        const moe_bf16 *x, const int32_t *local_experts,
+                        const moe_weights *weights, int64_t *counts,
+                        moe_bf16 *out, const moe_taps *taps, void *stream);
 
 /*
  * ---- Source-aware expert placement (Sec. 5.2 objective, Sec. 5.3 greedy) ---

@@ -244,6 +244,30 @@ int run_ffn(const moe_dims* d, const uint16_t* x_perm, const int32_t* x_rows, co
   return MOE_OK;
 }
 
+// The workspace of moe_forward_noalloc: a library-owned device array, one
+// copy per device (every device the library runs on holds it until the
+// process ends).  Host code never uses its name as an address: the address
+// of a device's copy comes from hipGetSymbolAddress on that device.
+static __device__ __align__(256) unsigned char scratch[MOE_NOALLOC_SCRATCH_BYTES];
+
+// The device address of the current device's copy of `scratch`, looked up
+// once per device (the pointers are cached with atomic operations, so
+// concurrent first calls are safe); nullptr when the lookup fails.
+void* scratch_address() {
+  constexpr int kMaxDevices = 64;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  void* p = __atomic_load_n(&addr[dev], __ATOMIC_ACQUIRE);
+  if (p != nullptr) return p;
+  if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  __atomic_store_n(&addr[dev], p, __ATOMIC_RELEASE);
+  return p;
+}
+
 }  // namespace
 
 extern "C" {
@@ -416,6 +440,27 @@ int moe_forward(const moe_dims* d, const moe_gating* gating, const float* logits
   if (e != hipSuccess) return MOE_ERR_DEVICE;
   record(taps, 2 * MOE_STAGE_COMBINE + 1, st);
   return MOE_OK;
+}
+
+int moe_forward_noalloc(const moe_dims* d, const moe_gating* gating, const float* logits, const int32_t* src,
+                        const moe_bf16* x, const int32_t* local_experts, const moe_weights* w, int64_t* counts,
+                        moe_bf16* out, const moe_taps* taps, void* stream) {
+  int s = check_dims(d);
+  if (s != MOE_OK) return s;
+  s = check_entry(d, MOE_ENTRY_FORWARD);
+  if (s != MOE_OK) return s;
+  if (entry_ws(d, MOE_ENTRY_FORWARD) > MOE_NOALLOC_SCRATCH_BYTES) return MOE_ERR_WORKSPACE;
+  // the scratch copy used is the current device's: the stream must be one of its streams
+  int cur = 0, sdev = 0;
+  if (hipGetDevice(&cur) != hipSuccess || hipStreamGetDevice(static_cast<hipStream_t>(stream), &sdev) != hipSuccess ||
+      cur != sdev)
+    return MOE_ERR_DEVICE;
+  void* ws = scratch_address();
+  if (ws == nullptr) return MOE_ERR_DEVICE;
+  // the forward workspace needs no initialisation: every region is written
+  // before it is read within the call
+  return moe_forward(d, gating, logits, src, x, local_experts, w, counts, out, taps, ws,
+                     MOE_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 size_t moe_place_slots(const moe_place_dims* pd, const int32_t* cap) {

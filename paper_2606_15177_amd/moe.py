@@ -78,6 +78,8 @@ def _load() -> C.CDLL:
         "moe_combine": ([dp, vp, vp, vp, vp, vp, vp], i32),
         "moe_forward": ([dp, C.POINTER(MoeGating), vp, vp, vp, vp, C.POINTER(MoeWeights), vp, vp,
                          C.POINTER(MoeTaps), vp, sz, vp], i32),
+        "moe_forward_noalloc": ([dp, C.POINTER(MoeGating), vp, vp, vp, vp, C.POINTER(MoeWeights), vp, vp,
+                                 C.POINTER(MoeTaps), vp], i32),
         "moe_place_slots": ([C.POINTER(MoePlaceDims), vp], sz),
         "moe_place_experts": ([C.POINTER(MoePlaceDims), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp], i32),
         "moe_window_stats": ([C.POINTER(MoeWindowDims), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp], i32),
@@ -222,6 +224,16 @@ def forward(d, logits, src, x, local_experts, weights, counts, out, ws, taps=Non
                             _ptr(out, _BF16), None if taps is None else C.byref(taps), _ptr(ws),
                             0 if ws is None else ws.numel() * ws.element_size(), _stream(stream)),
            "moe_forward")
+
+
+def forward_noalloc(d, logits, src, x, local_experts, weights, counts, out, taps=None, stream=None, gating=None):
+    """moe_forward_noalloc: the layer with the library's own scratch array as
+    its workspace (no workspace argument, nothing allocated)."""
+    w = weights if isinstance(weights, MoeWeights) else make_weights(weights)
+    _check(_lib.moe_forward_noalloc(C.byref(d), _gating_ref(gating), _ptr(logits, _F32), _ptr(src, _I32),
+                                    _ptr(x, _BF16), _ptr(local_experts, _I32), C.byref(w), _ptr(counts, _I64),
+                                    _ptr(out, _BF16), None if taps is None else C.byref(taps), _stream(stream)),
+           "moe_forward_noalloc")
 
 
 PAPER_PLACE_WEIGHTS = (1.0, 0.0025, 1.0)  # (alpha, beta, gamma), Sec. 6

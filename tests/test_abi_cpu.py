@@ -247,3 +247,18 @@ def test_kernel_limits_of_each_gemm(moe, change):
     assert moe.validate(d, moe.ENTRY_EXPERT_FFN, 1 << 62) == moe.MOE_ERR_UNSUPPORTED
     assert moe.validate(d, moe.ENTRY_FORWARD, 1 << 62) == moe.MOE_ERR_UNSUPPORTED
     assert moe.validate(d, moe.ENTRY_PERMUTE, 1 << 62) == moe.MOE_OK
+
+
+def test_forward_noalloc_rejects_on_the_host(moe):
+    """moe_forward_noalloc's workspace is the library's 32 MiB scratch array:
+    larger layers are refused before anything is enqueued."""
+    lib = moe._lib
+    w = moe.MoeWeights(256, 256, 256, 256, 256, 256)
+    assert lib.moe_forward_noalloc(None, None, 256, 256, 256, 256, C.byref(w), None, 256, None,
+                                   None) == moe.MOE_ERR_NULL
+    big = moe.dims_of(W.CONFIGS["ep_share_dsv3"])
+    assert moe.workspace_bytes(big, moe.ENTRY_FORWARD) > 32 << 20
+    assert lib.moe_forward_noalloc(C.byref(big), None, 256, 256, 256, 256, C.byref(w), None, 256, None,
+                                   None) == moe.MOE_ERR_WORKSPACE
+    decode = moe.dims_of(W.CONFIGS["decode_mixtral"])
+    assert moe.workspace_bytes(decode, moe.ENTRY_FORWARD) <= 32 << 20
