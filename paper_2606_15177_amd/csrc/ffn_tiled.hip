@@ -15,6 +15,11 @@
 // groups that end at or before the tile.  Group sizes never leave the
 // device.
 //
+// Tail tiles.  An expert whose rows past its last whole m-tile number 1..128
+// takes them in tiles of 128 token rows x 512 weight rows, each covering two
+// column tiles, with their own LDS layout and pipeline (see TAIL): half the
+// tiles that a padded 256-row m-tile would take.
+//
 // Two problems.  The shared experts (static rows: every token) can run in
 // the routed experts' launch: their tiles come first, and each load stream
 // and the epilogue follow the problem of the tile they are on.  This is used
@@ -139,7 +144,18 @@ struct TiledArgs {
 // m-tiles, n-tile-major inside a block: one XCD's 32 concurrent tiles are
 // then 8 m-tiles x 4 n-tiles, instead of 32 m-tiles of one n-tile, each of
 // whose token tiles would be fetched again for every n-tile.
-template <bool GATED, int kPfx, bool PAIR, bool SBLK>
+//
+// TAIL (grouped problems): a group whose rows past its last whole 256-row
+// m-tile number 1..128 runs them as tail tiles of 128 token rows x 512
+// weight rows (twice the columns of a full tile), half the tiles such a
+// padded last m-tile took.  Within a group the tiles go by pairs of
+// column tiles: the full tiles of column tiles 2p and 2p + 1 (m-tiles
+// fastest), then the tail tile that covers both, so the tail tile runs
+// beside the full tiles that read the same weight rows.  A tail tile has
+// its own LDS layout (two 80 KB stages: X [128 x 64], W [512 x 64]) and
+// pipeline; a workgroup drains its pipeline where its sequence of tiles
+// switches between the two kinds.
+template <bool GATED, int kPfx, bool PAIR, bool SBLK, bool TAIL>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void tiled_kernel(TiledArgs ta) {
   using C = Stage;
   const GemmArgs& a = ta.g;
@@ -158,10 +174,17 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   const int wm = wave & 3, wn = wave >> 2;
   const int lrow = lane & 31, lhalf = lane >> 5;
   const int n_tiles_n = ceil_div(a.N, OUT_COLS);
+  const int n_tiles_t = ceil_div(n_tiles_n, 2);  // column tiles of a tail tile (512 weight rows)
 
-  // m-tile prefix of the groups, in registers: lane L holds the end (one
-  // past the last m-tile) of groups L + 64 i, i < kPfx; groups past the end
-  // hold INT_MAX
+  // full m-tiles and tail tiles of a group of n rows
+  auto group_shape = [&](int n, int& fm, int& tl) {
+    const int rem = n % kBM;
+    tl = (TAIL && rem > 0 && rem <= kBM / 2) ? 1 : 0;
+    fm = n / kBM + ((rem > 0 && !tl) ? 1 : 0);
+  };
+  // tile prefix of the groups, in registers: lane L holds the end (one past
+  // the last tile; without TAIL, the last m-tile) of groups L + 64 i,
+  // i < kPfx; groups past the end hold INT_MAX
   int mt_end[kPfx];
   int total_mt;
   if (a.offsets == nullptr) {
@@ -174,7 +197,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     for (int i = 0; i < kPfx; ++i) {
       const int g = i * kWave + lane;
       int cnt = 0;
-      if (i * kWave < a.groups && g < a.groups) cnt = ceil_div(a.offsets[g + 1] - a.offsets[g], kBM);
+      if (i * kWave < a.groups && g < a.groups) {
+        const int n = a.offsets[g + 1] - a.offsets[g];
+        if constexpr (TAIL) {
+          int fm, tl;
+          group_shape(n, fm, tl);
+          cnt = fm * n_tiles_n + tl * n_tiles_t;
+        } else {
+          cnt = ceil_div(n, kBM);
+        }
+      }
       int inc = cnt;
 #pragma unroll
       for (int off = 1; off < kWave; off <<= 1) {
@@ -186,7 +218,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     }
     total_mt = carry;
   }
-  const int total_tiles = sp_tiles + total_mt * n_tiles_n;
+  // tiles of g: with TAIL the prefix already counts tiles
+  const int total_tiles = sp_tiles + ((TAIL && a.offsets != nullptr) ? total_mt : total_mt * n_tiles_n);
   const int per_xcd = gridDim.x / 8;
   const int first = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
   if (first >= total_tiles) return;
@@ -194,10 +227,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 
   struct TileInfo {
     int p, g, row_base, m, m0, nt;  // p: 0 for sp, 1 for g
+    bool tail;                      // a tail tile (nt then counts 512-row column tiles)
   };
   // group of tile t: the number of groups whose tiles all precede t
   auto tile_info = [&](int t_all) {
     TileInfo ti;
+    ti.tail = false;
     ti.p = (PAIR && t_all < sp_tiles) ? 0 : 1;
     const int t = ti.p ? t_all - sp_tiles : t_all;
     int mg = ti.p ? total_mt : sp_mt, base = 0;
@@ -205,11 +240,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     ti.row_base = 0;
     ti.m = ti.p ? a.static_rows : sp.static_rows;
     if (ti.p && a.offsets != nullptr) {
+      constexpr int kScale = 1;
+      const int scale = TAIL ? kScale : n_tiles_n;
       int cnt = 0, lo = 0, hi = 0x7fffffff;
 #pragma unroll
       for (int i = 0; i < kPfx; ++i) {
         const int e = mt_end[i];
-        const bool before = e != 0x7fffffff && e * n_tiles_n <= t;
+        const bool before = e != 0x7fffffff && e * scale <= t;
         cnt += before ? 1 : 0;
         lo = before ? max(lo, e) : lo;
         hi = before ? hi : min(hi, e);
@@ -221,8 +258,30 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       ti.g = g;
       ti.row_base = a.offsets[g];
       ti.m = a.offsets[g + 1] - ti.row_base;
-      base = __builtin_amdgcn_readfirstlane(lo) * n_tiles_n;
+      base = __builtin_amdgcn_readfirstlane(lo) * scale;
       mg = __builtin_amdgcn_readfirstlane(hi) - __builtin_amdgcn_readfirstlane(lo);
+      if constexpr (TAIL) {
+        // pairs of column tiles: the full tiles of columns 2p and 2p + 1
+        // (m-tiles fastest), then the tail tile of pair p
+        int fm, tl;
+        group_shape(ti.m, fm, tl);
+        const int local = t - base;
+        const int per_pair = 2 * fm + tl;
+        const int pr = min(local / max(per_pair, 1), n_tiles_t - 1);
+        const int r = local - pr * per_pair;
+        const int nfull = min(2, n_tiles_n - 2 * pr) * fm;
+        const int fmd = max(fm, 1);
+        ti.tail = r >= nfull;
+        ti.nt = ti.tail ? pr : 2 * pr + r / fmd;
+        ti.m0 = (ti.tail ? fm : r % fmd) * kBM;
+        ti.tail = __builtin_amdgcn_readfirstlane(ti.tail ? 1 : 0) != 0;
+        ti.g = __builtin_amdgcn_readfirstlane(ti.g);
+        ti.row_base = __builtin_amdgcn_readfirstlane(ti.row_base);
+        ti.m = __builtin_amdgcn_readfirstlane(ti.m);
+        ti.m0 = __builtin_amdgcn_readfirstlane(ti.m0);
+        ti.nt = __builtin_amdgcn_readfirstlane(ti.nt);
+        return ti;
+      }
     }
     const int local = t - base;
     if constexpr (SBLK) {
@@ -262,110 +321,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   };
   // the 32 weight rows of this wave are all gate rows or all up rows
   const bool w_up = GATED && ((wave >> 1) & 1);
-  __amdgpu_buffer_rsrc_t rs_x, rs_w;
-  uint32_t xoff[C::LPP], woff[C::LPP];
-  int x_tile = first, x_kb = 0, w_tile = first, w_kb = 0;
-  int x_p = 1, w_p = 1, x_nkb = 1, w_nkb = 1;  // each stream's problem and its K stages
-  uint32_t kx0 = 0, kx1 = 0, kw0 = 0, kw1 = 0;
+  // the workgroup's current run of tiles of one kind: its first tile and the
+  // first tile of its sequence past the run (loads past it are dead: no
+  // traffic)
+  int run_start = first, run_end = total_tiles;
   auto prob = [&](int p) -> const GemmArgs& { return (!PAIR || p) ? a : sp; };
   const int nkb_g = ceil_div(a.K, C::BK);
-
-  auto x_setup = [&](int t_in) {
-    const bool live = t_in < total_tiles;
-    const uint32_t dead = live ? 0u : kInvalid;
-    const int t = live ? t_in : total_tiles - 1;
-    const TileInfo ti = tile_info(t);
-    x_p = PAIR ? ti.p : 1;
-    const GemmArgs& q = prob(x_p);
-    x_nkb = PAIR ? ceil_div(q.K, C::BK) : nkb_g;
-    const int ln = opaque_lane_id();
-    const uint16_t* xb = q.x_rows ? q.x : q.x + static_cast<size_t>(ti.row_base + ti.m0) * q.K;
-    rs_x = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(xb), 0, kRecords, kRsrcWord3);
-    int xr[C::LPP];
-#pragma unroll
-    for (int i = 0; i < C::LPP; ++i) {
-      const int r = 32 * wave + C::RPI * i + ln / C::CPR;
-      xr[i] = r;
-      if (q.x_rows) xr[i] = q.x_rows[ti.row_base + (ti.m0 + r < ti.m ? ti.m0 + r : 0)];
-    }
-#pragma unroll
-    for (int i = 0; i < C::LPP; ++i) {
-      const int r = 32 * wave + C::RPI * i + ln / C::CPR;
-      xoff[i] = (ti.m0 + r < ti.m ? static_cast<uint32_t>(xr[i] * q.K * 2 + chunk_of(i, ln) * 16) : kInvalid) | dead;
-    }
-  };
-  auto w_setup = [&](int t_in) {
-    const bool live = t_in < total_tiles;
-    const uint32_t dead = live ? 0u : kInvalid;
-    const int t = live ? t_in : total_tiles - 1;
-    const TileInfo ti = tile_info(t);
-    w_p = PAIR ? ti.p : 1;
-    const GemmArgs& q = prob(w_p);
-    w_nkb = PAIR ? ceil_div(q.K, C::BK) : nkb_g;
-    const int ln = opaque_lane_id();
-    const int col0 = ti.nt * OUT_COLS;
-    const size_t gofs = static_cast<size_t>(ti.g) * q.group_stride + static_cast<size_t>(col0) * q.ldw;
-    rs_w = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>((w_up ? q.w1 : q.w0) + gofs), 0, kRecords, kRsrcWord3);
-#pragma unroll
-    for (int i = 0; i < C::LPP; ++i) {
-      const int r = 32 * wave + C::RPI * i + ln / C::CPR;
-      const int lcol = GATED ? (r >> 7) * 64 + (r & 63) : r;
-      woff[i] = ((col0 + lcol < q.N) ? static_cast<uint32_t>(lcol * q.ldw * 2 + chunk_of(i, ln) * 16) : kInvalid) | dead;
-    }
-  };
   auto kmask = [&](int kb, int p, int K) { return kb * C::BK + chunk_of(p, lane) * 8 < K ? 0u : kInvalid; };
-  auto x_kstep = [&]() {
-    const uint32_t k = static_cast<uint32_t>(x_kb * C::BK * 2);
-    const int K = prob(x_p).K;
-    kx0 = k | kmask(x_kb, 0, K);
-    kx1 = k | kmask(x_kb, 1, K);
-  };
-  auto w_kone = [&](int p) -> uint32_t {
-    const GemmArgs& q = prob(w_p);
-    const int k0 = w_kb * C::BK;
-    uint32_t w;
-    if (q.kseg >= q.K) {
-      w = static_cast<uint32_t>(k0 * 2);
-    } else if (q.kseg % C::BK == 0) {
-      const int seg = k0 / q.kseg;
-      w = static_cast<uint32_t>((static_cast<size_t>(seg) * q.seg_stride + (k0 - seg * q.kseg)) * 2);
-    } else {
-      const int kk = min(k0 + chunk_of(p, lane) * 8, q.K - 8);
-      w = static_cast<uint32_t>((weight_col_offset(q, kk) - static_cast<size_t>(kk - k0)) * 2);
-    }
-    return w | kmask(w_kb, p, q.K);
-  };
-  auto w_kstep = [&]() {
-    kw0 = w_kone(0);
-    kw1 = w_kone(1);
-  };
-  auto x_advance = [&]() {
-    if (++x_kb == (PAIR ? x_nkb : nkb_g)) {
-      x_kb = 0;
-      x_tile += gridDim.x;
-      x_setup(x_tile);
-    }
-    x_kstep();
-  };
-  auto w_advance = [&]() {
-    if (++w_kb == (PAIR ? w_nkb : nkb_g)) {
-      w_kb = 0;
-      w_tile += gridDim.x;
-      w_setup(w_tile);
-    }
-    w_kstep();
-  };
   // part P (X of stage s: 2s, W of stage s: 2s + 1) lives in slot P % 5
   auto part_ptr = [&](int P) { return smem + (P % C::NPARTS) * C::PART; };
-  auto x_load = [&](int s, int i) {
-    const uint32_t k = (i & 1) ? kx1 : kx0;
-    load_lds16(rs_x, part_ptr(2 * s) + wave * (32 * C::ROW) + i * 1024, (xoff[i] + k) | (k & kInvalid));
-  };
-  auto w_load = [&](int s, int i) {
-    const uint32_t k = (i & 1) ? kw1 : kw0;
-    load_lds16(rs_w, part_ptr(2 * s + 1) + wave * (32 * C::ROW) + i * 1024, (woff[i] + k) | (k & kInvalid));
-  };
-
   // ---- compute side ----
   const int xrow0 = wm * 64, wrow0 = wn * 128;
   const int rsw = (lrow / C::SWZ) % C::CPR;
@@ -394,12 +358,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 #pragma unroll
       for (int tm = 0; tm < 2; ++tm) acc[tn][tm] = f32x16{};
   };
-  auto epilogue = [&](const TileInfo& ti) {
+  // the wave's output columns: WCOLS of them from col_w; rows from xr0
+  constexpr int WCOLS = GATED ? 64 : 128;
+  auto epilogue = [&](const TileInfo& ti, int xr0, int col_w) {
     const GemmArgs& pr = prob(ti.p);
     const int ln = opaque_lane_id();
     const int erow = ln & 31, ehalf = ln >> 5;
-    constexpr int WCOLS = GATED ? 64 : 128;
-    const int col_w = ti.nt * OUT_COLS + wn * WCOLS;
     // The tile's output rows through a buffer descriptor: rows past the
     // group and columns past N get offsets >= 2^31, which the hardware
     // drops, so the stores need no branches and the conversions of all of
@@ -408,7 +372,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         pr.out + static_cast<size_t>(ti.row_base + ti.m0) * pr.N, 0, kRecords, kRsrcWord3);
 #pragma unroll
     for (int tm = 0; tm < 2; ++tm) {
-      const int r = xrow0 + tm * 32 + erow;  // row within the tile
+      const int r = xr0 + tm * 32 + erow;  // row within the tile
       const uint32_t row_off = ti.m0 + r < ti.m ? static_cast<uint32_t>(r * pr.N * 2) : kInvalid;
       constexpr int TOUT = GATED ? 2 : 4;
 #pragma unroll
@@ -444,7 +408,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     }
   };
 
-  // ---- pipeline ----
+  // ---- pipeline of full tiles ----
   // Stage j: barrier before its last K-step, after every wave's last LDS
   // read of the stage.  Past barrier j - 1 the slot of X of stage j - 1
   // takes W of stage j + 1 (first half among the MFMAs of stage j - 1's last
@@ -452,61 +416,305 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   // of stage j - 1 takes X of stage j + 2 (among the MFMAs of stage j's
   // K-steps 1 and 2).  Before barrier j each wave waits for its loads of
   // stage j + 1; only X of stage j + 2 may still be in flight.
-  zero_acc();
-  x_setup(first);
-  x_kstep();
-  w_setup(first);
-  w_kstep();
-  // stages 0 and 1, but only the first half of W of stage 1 (its second
-  // half goes out with stage 0's first K-step)
-  for (int s = 0; s < 2; ++s) {
+  auto full_run = [&]() {
+    __amdgpu_buffer_rsrc_t rs_x, rs_w;
+    uint32_t xoff[C::LPP], woff[C::LPP];
+    int x_tile = first, x_kb = 0, w_tile = first, w_kb = 0;
+    int x_p = 1, w_p = 1, x_nkb = 1, w_nkb = 1;  // each stream's problem and its K stages
+    uint32_t kx0 = 0, kx1 = 0, kw0 = 0, kw1 = 0;
+
+    auto x_setup = [&](int t_in) {
+      const bool live = t_in < run_end;
+      const uint32_t dead = live ? 0u : kInvalid;
+      const int t = live ? t_in : run_start;
+      const TileInfo ti = tile_info(t);
+      x_p = PAIR ? ti.p : 1;
+      const GemmArgs& q = prob(x_p);
+      x_nkb = PAIR ? ceil_div(q.K, C::BK) : nkb_g;
+      const int ln = opaque_lane_id();
+      const uint16_t* xb = q.x_rows ? q.x : q.x + static_cast<size_t>(ti.row_base + ti.m0) * q.K;
+      rs_x = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(xb), 0, kRecords, kRsrcWord3);
+      int xr[C::LPP];
 #pragma unroll
-    for (int i = 0; i < C::LPP; ++i) x_load(s, i);
-    x_advance();
+      for (int i = 0; i < C::LPP; ++i) {
+        const int r = 32 * wave + C::RPI * i + ln / C::CPR;
+        xr[i] = r;
+        if (q.x_rows) xr[i] = q.x_rows[ti.row_base + (ti.m0 + r < ti.m ? ti.m0 + r : 0)];
+      }
 #pragma unroll
-    for (int i = 0; i < C::LPP; ++i)
-      if (s == 0 || i < C::LPP / 2) w_load(s, i);
-    if (s == 0) w_advance();
-  }
-  __builtin_amdgcn_s_waitcnt(wait_vm(C::LPP + C::LPP / 2));  // own stage-0 loads landed
-  phase_barrier();
-  read_frags(0, 0, 0);
-  int j = 0;
-  for (int t = first; t < total_tiles; t += gridDim.x) {
-    const TileInfo cur = tile_info(t);  // scalars, held through the K loop
-    const int nkb = PAIR ? ceil_div(prob(cur.p).K, C::BK) : nkb_g;
-    for (int kb = 0; kb < nkb; ++kb, ++j) {
-      // K-step 0 with the second half of W of stage j + 1, K-steps 1 and 2
-      // with X of stage j + 2: two loads per wave and K-step
+      for (int i = 0; i < C::LPP; ++i) {
+        const int r = 32 * wave + C::RPI * i + ln / C::CPR;
+        xoff[i] = (ti.m0 + r < ti.m ? static_cast<uint32_t>(xr[i] * q.K * 2 + chunk_of(i, ln) * 16) : kInvalid) | dead;
+      }
+    };
+    auto w_setup = [&](int t_in) {
+      const bool live = t_in < run_end;
+      const uint32_t dead = live ? 0u : kInvalid;
+      const int t = live ? t_in : run_start;
+      const TileInfo ti = tile_info(t);
+      w_p = PAIR ? ti.p : 1;
+      const GemmArgs& q = prob(w_p);
+      w_nkb = PAIR ? ceil_div(q.K, C::BK) : nkb_g;
+      const int ln = opaque_lane_id();
+      const int col0 = ti.nt * OUT_COLS;
+      const size_t gofs = static_cast<size_t>(ti.g) * q.group_stride + static_cast<size_t>(col0) * q.ldw;
+      rs_w = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>((w_up ? q.w1 : q.w0) + gofs), 0, kRecords, kRsrcWord3);
 #pragma unroll
-      for (int ks = 0; ks < C::KSTEPS - 1; ++ks) {
-        read_frags(j, ks + 1, (ks + 1) & 1);
+      for (int i = 0; i < C::LPP; ++i) {
+        const int r = 32 * wave + C::RPI * i + ln / C::CPR;
+        const int lcol = GATED ? (r >> 7) * 64 + (r & 63) : r;
+        woff[i] = ((col0 + lcol < q.N) ? static_cast<uint32_t>(lcol * q.ldw * 2 + chunk_of(i, ln) * 16) : kInvalid) | dead;
+      }
+    };
+    auto x_kstep = [&]() {
+      const uint32_t k = static_cast<uint32_t>(x_kb * C::BK * 2);
+      const int K = prob(x_p).K;
+      kx0 = k | kmask(x_kb, 0, K);
+      kx1 = k | kmask(x_kb, 1, K);
+    };
+    auto w_kone = [&](int p) -> uint32_t {
+      const GemmArgs& q = prob(w_p);
+      const int k0 = w_kb * C::BK;
+      uint32_t w;
+      if (q.kseg >= q.K) {
+        w = static_cast<uint32_t>(k0 * 2);
+      } else if (q.kseg % C::BK == 0) {
+        const int seg = k0 / q.kseg;
+        w = static_cast<uint32_t>((static_cast<size_t>(seg) * q.seg_stride + (k0 - seg * q.kseg)) * 2);
+      } else {
+        const int kk = min(k0 + chunk_of(p, lane) * 8, q.K - 8);
+        w = static_cast<uint32_t>((weight_col_offset(q, kk) - static_cast<size_t>(kk - k0)) * 2);
+      }
+      return w | kmask(w_kb, p, q.K);
+    };
+    auto w_kstep = [&]() {
+      kw0 = w_kone(0);
+      kw1 = w_kone(1);
+    };
+    auto x_advance = [&]() {
+      if (++x_kb == (PAIR ? x_nkb : nkb_g)) {
+        x_kb = 0;
+        x_tile += gridDim.x;
+        x_setup(x_tile);
+      }
+      x_kstep();
+    };
+    auto w_advance = [&]() {
+      if (++w_kb == (PAIR ? w_nkb : nkb_g)) {
+        w_kb = 0;
+        w_tile += gridDim.x;
+        w_setup(w_tile);
+      }
+      w_kstep();
+    };
+    auto x_load = [&](int s, int i) {
+      const uint32_t k = (i & 1) ? kx1 : kx0;
+      load_lds16(rs_x, part_ptr(2 * s) + wave * (32 * C::ROW) + i * 1024, (xoff[i] + k) | (k & kInvalid));
+    };
+    auto w_load = [&](int s, int i) {
+      const uint32_t k = (i & 1) ? kw1 : kw0;
+      load_lds16(rs_w, part_ptr(2 * s + 1) + wave * (32 * C::ROW) + i * 1024, (woff[i] + k) | (k & kInvalid));
+    };
+    zero_acc();
+    x_tile = w_tile = run_start;
+    x_kb = w_kb = 0;
+    x_setup(run_start);
+    x_kstep();
+    w_setup(run_start);
+    w_kstep();
+    // stages 0 and 1, but only the first half of W of stage 1 (its second
+    // half goes out with stage 0's first K-step)
+    for (int s = 0; s < 2; ++s) {
 #pragma unroll
-        for (int i = 0; i < C::LPP / 2; ++i) {
-          if (ks == 0)
-            w_load(j + 1, C::LPP / 2 + i);
-          else
-            x_load(j + 2, (ks - 1) * (C::LPP / 2) + i);
+      for (int i = 0; i < C::LPP; ++i) x_load(s, i);
+      x_advance();
+#pragma unroll
+      for (int i = 0; i < C::LPP; ++i)
+        if (s == 0 || i < C::LPP / 2) w_load(s, i);
+      if (s == 0) w_advance();
+    }
+    __builtin_amdgcn_s_waitcnt(wait_vm(C::LPP + C::LPP / 2));  // own stage-0 loads landed
+    phase_barrier();
+    read_frags(0, 0, 0);
+    int j = 0;
+    for (int t = run_start; t < run_end; t += gridDim.x) {
+      const TileInfo cur = tile_info(t);  // scalars, held through the K loop
+      const int nkb = PAIR ? ceil_div(prob(cur.p).K, C::BK) : nkb_g;
+      for (int kb = 0; kb < nkb; ++kb, ++j) {
+        // K-step 0 with the second half of W of stage j + 1, K-steps 1 and 2
+        // with X of stage j + 2: two loads per wave and K-step
+#pragma unroll
+        for (int ks = 0; ks < C::KSTEPS - 1; ++ks) {
+          read_frags(j, ks + 1, (ks + 1) & 1);
+#pragma unroll
+          for (int i = 0; i < C::LPP / 2; ++i) {
+            if (ks == 0)
+              w_load(j + 1, C::LPP / 2 + i);
+            else
+              x_load(j + 2, (ks - 1) * (C::LPP / 2) + i);
+          }
+          if (ks == 0) w_advance();
+          mfma_set(ks & 1);
+          __builtin_amdgcn_sched_barrier(0);
         }
-        if (ks == 0) w_advance();
-        mfma_set(ks & 1);
+        x_advance();
+        __builtin_amdgcn_s_waitcnt(wait_vm(C::LPP));  // own stage j+1 landed
+        __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+        phase_barrier();
+        // last K-step with the first half of W of stage j + 2
+        read_frags(j + 1, 0, 0);  // past the last stage: a harmless stale read
+#pragma unroll
+        for (int i = 0; i < C::LPP / 2; ++i) w_load(j + 2, i);
+        mfma_set((C::KSTEPS - 1) & 1);
         __builtin_amdgcn_sched_barrier(0);
       }
-      x_advance();
-      __builtin_amdgcn_s_waitcnt(wait_vm(C::LPP));  // own stage j+1 landed
-      __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
-      phase_barrier();
-      // last K-step with the first half of W of stage j + 2
-      read_frags(j + 1, 0, 0);  // past the last stage: a harmless stale read
-#pragma unroll
-      for (int i = 0; i < C::LPP / 2; ++i) w_load(j + 2, i);
-      mfma_set((C::KSTEPS - 1) & 1);
-      __builtin_amdgcn_sched_barrier(0);
+      epilogue(cur, xrow0, cur.nt * OUT_COLS + wn * WCOLS);
+      zero_acc();
     }
-    epilogue(cur);
+  };
+
+  // ---- tail tiles: 128 token rows x 512 weight rows ----
+  // Two stages of 80 KB: X [128 rows x 128 B] at 0, W [512 rows x 128 B] at
+  // 16 KB, the same chunk swizzle as the full parts.  Wave w fills X rows
+  // 16w .. 16w+15 (two loads) and W rows 64w .. 64w+63 (eight loads, all
+  // gate or all up rows); wave (wm_t, wn_t) = (w & 1, w >> 1) owns token rows
+  // 64 wm_t .. +63 and weight rows 128 wn_t .. +127, the same 2 x 4 MFMA
+  // tiles as in a full tile.  The loads of stage j + 1 go out among the
+  // first MFMAs of stage j into the other stage buffer, read last in stage
+  // j - 1.  (Stages of 32 along K, four in flight in 40 KB buffers, were
+  // measured no faster.)
+  constexpr int T_XROWS = kBM / 2, T_WROWS = 2 * kBN;
+  constexpr int T_XPART = T_XROWS * C::ROW;             // 16 KB
+  constexpr int T_STAGE = T_XPART + T_WROWS * C::ROW;   // 80 KB
+  constexpr int T_XL = T_XROWS / C::RPI / 8;            // X loads per wave and stage: 2
+  constexpr int T_WL = T_WROWS / C::RPI / 8;            // W loads per wave and stage: 8
+  constexpr int OUT_COLS_T = 2 * OUT_COLS;
+  static_assert(2 * T_STAGE <= C::LDS, "two tail stages fit the LDS");
+  const int wm_t = wave & 1, wn_t = wave >> 1;
+  const int xrow0_t = wm_t * 64, wrow0_t = wn_t * 128;
+  auto t_buf = [&](int b) { return smem + b * T_STAGE; };
+  auto t_read_frags = [&](int b, int ks, int set) {
+    const unsigned char* xp = t_buf(b);
+    const unsigned char* wp = xp + T_XPART;
+    const int slot = ((2 * ks + lhalf) ^ rsw) << 4;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      wf[set][t] = as_bf16x8(*reinterpret_cast<const u32x4*>(wp + (wrow0_t + t * 32 + lrow) * C::ROW + slot));
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+      xf[set][t] = as_bf16x8(*reinterpret_cast<const u32x4*>(xp + (xrow0_t + t * 32 + lrow) * C::ROW + slot));
+  };
+  auto tail_run = [&]() {
+    __amdgpu_buffer_rsrc_t trs_x, trs_w;
+    uint32_t txoff[T_XL], twoff[T_WL];
+    int tt = first, tkb = 0;
+    uint32_t tk0 = 0, tk1 = 0;
+    auto t_setup = [&](int t_in) {
+      const bool live = t_in < run_end;
+      const uint32_t dead = live ? 0u : kInvalid;
+      const TileInfo ti = tile_info(live ? t_in : run_start);
+      const int ln = opaque_lane_id();
+      const uint16_t* xb = a.x_rows ? a.x : a.x + static_cast<size_t>(ti.row_base + ti.m0) * a.K;
+      trs_x = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(xb), 0, kRecords, kRsrcWord3);
+#pragma unroll
+      for (int i = 0; i < T_XL; ++i) {
+        const int r = 16 * wave + C::RPI * i + ln / C::CPR;
+        const bool in = ti.m0 + r < ti.m;
+        const int xr = a.x_rows ? a.x_rows[ti.row_base + (in ? ti.m0 + r : 0)] : r;
+        txoff[i] = (in ? static_cast<uint32_t>(xr * a.K * 2 + chunk_of(i, ln) * 16) : kInvalid) | dead;
+      }
+      const int col0 = ti.nt * OUT_COLS_T;
+      const size_t gofs = static_cast<size_t>(ti.g) * a.group_stride + static_cast<size_t>(col0) * a.ldw;
+      const bool up = GATED && (wave & 1);  // W rows 64w .. 64w+63: gate rows for even w, up rows for odd w
+      trs_w = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>((up ? a.w1 : a.w0) + gofs), 0, kRecords,
+                                                kRsrcWord3);
+#pragma unroll
+      for (int i = 0; i < T_WL; ++i) {
+        const int r = 64 * wave + C::RPI * i + ln / C::CPR;
+        const int lcol = GATED ? (r >> 7) * 64 + (r & 63) : r;
+        twoff[i] =
+            ((col0 + lcol < a.N) ? static_cast<uint32_t>(lcol * a.ldw * 2 + chunk_of(i, ln) * 16) : kInvalid) | dead;
+      }
+    };
+    auto t_kstep = [&]() {
+      const uint32_t k = static_cast<uint32_t>(tkb * C::BK * 2);
+      tk0 = k | kmask(tkb, 0, a.K);
+      tk1 = k | kmask(tkb, 1, a.K);
+    };
+    auto t_advance = [&]() {
+      if (++tkb == nkb_g) {
+        tkb = 0;
+        tt += gridDim.x;
+        t_setup(tt);
+      }
+      t_kstep();
+    };
+    auto t_load = [&](int b, int i) {  // load i < T_XL: X, else W load i - T_XL
+      const uint32_t k = (i & 1) ? tk1 : tk0;
+      if (i < T_XL)
+        load_lds16(trs_x, t_buf(b) + wave * (16 * C::ROW) + i * 1024, (txoff[i] + k) | (k & kInvalid));
+      else
+        load_lds16(trs_w, t_buf(b) + T_XPART + wave * (64 * C::ROW) + (i - T_XL) * 1024,
+                   (twoff[i - T_XL] + k) | (k & kInvalid));
+    };
     zero_acc();
+    tt = run_start;
+    tkb = 0;
+    t_setup(tt);
+    t_kstep();
+#pragma unroll
+    for (int i = 0; i < T_XL + T_WL; ++i) t_load(0, i);
+    t_advance();
+    __builtin_amdgcn_s_waitcnt(kWaitAll);
+    phase_barrier();
+    int j = 0;
+    for (int t = run_start; t < run_end; t += gridDim.x) {
+      const TileInfo cur = tile_info(t);
+      for (int kb = 0; kb < nkb_g; ++kb, ++j) {
+        const int b = j & 1;
+        t_read_frags(b, 0, 0);
+#pragma unroll
+        for (int ks = 0; ks < C::KSTEPS; ++ks) {
+          if (ks + 1 < C::KSTEPS) t_read_frags(b, ks + 1, (ks + 1) & 1);
+          // stage j + 1's ten loads in the first three K-steps (4, 4, 2),
+          // so that they have landed by the end of the stage
+          constexpr int kFirst[5] = {0, 4, 8, 10, 10};
+#pragma unroll
+          for (int i = kFirst[ks]; i < kFirst[ks + 1]; ++i) t_load(b ^ 1, i);
+          mfma_set(ks & 1);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        t_advance();
+        __builtin_amdgcn_s_waitcnt(kWaitAll);  // own stage j+1 landed, LDS reads done
+        phase_barrier();
+      }
+      epilogue(cur, xrow0_t, cur.nt * OUT_COLS_T + wn_t * WCOLS);
+      zero_acc();
+    }
+  };
+
+  // ---- runs ----
+  // The workgroup walks its tiles t, t + gridDim, ... in runs of one kind;
+  // between runs every load has landed and every wave has passed a barrier,
+  // so the next run may refill the LDS from scratch.
+  for (int t = first; t < total_tiles;) {
+    const bool tail = TAIL && tile_info(t).tail;
+    int e = t;
+    if constexpr (TAIL) {
+      while (e < total_tiles && tile_info(e).tail == tail) e += gridDim.x;
+    } else {
+      e = total_tiles;
+    }
+    run_start = t;
+    run_end = e;
+    if (TAIL && tail)
+      tail_run();
+    else
+      full_run();
+    __builtin_amdgcn_s_waitcnt(kWaitAll);
+    phase_barrier();
+    t = e;
   }
-  __builtin_amdgcn_s_waitcnt(kWaitAll);
 }
 
 // Compute units of the current device, looked up once per device: a
@@ -526,25 +734,33 @@ int device_cu_count() {
   return n;
 }
 
-template <bool GATED, int PFX, bool PAIR, bool SBLK>
+template <bool GATED, int PFX, bool PAIR, bool SBLK, bool TAIL>
 hipError_t launch_pfx_t(const TiledArgs& ta, long long grid, hipStream_t st) {
   static unsigned long long lds_set = 0;  // devices with the LDS limit raised
   const hipError_t e_lds =
-      set_max_dynamic_lds(reinterpret_cast<const void*>(&tiled_kernel<GATED, PFX, PAIR, SBLK>),
+      set_max_dynamic_lds(reinterpret_cast<const void*>(&tiled_kernel<GATED, PFX, PAIR, SBLK, TAIL>),
                           Stage::LDS, &lds_set);
   if (e_lds != hipSuccess) return e_lds;
-  hipLaunchKernelGGL((tiled_kernel<GATED, PFX, PAIR, SBLK>), dim3(static_cast<unsigned>(grid)), dim3(kThreads),
-                     Stage::LDS, st, ta);
+  hipLaunchKernelGGL((tiled_kernel<GATED, PFX, PAIR, SBLK, TAIL>), dim3(static_cast<unsigned>(grid)),
+                     dim3(kThreads), Stage::LDS, st, ta);
   return hipGetLastError();
 }
 
+// Grouped problems (device offsets) take the kernel with tail tiles; a
+// launch of static rows alone takes the blocked tile order.
 template <bool GATED, int PFX>
 hipError_t launch_pfx(const TiledArgs& ta, long long grid, hipStream_t st) {
-  if (ta.sp_tiles > 0) return launch_pfx_t<GATED, PFX, true, false>(ta, grid, st);
-  if constexpr (PFX == 1) {
-    if (ta.g.offsets == nullptr) return launch_pfx_t<GATED, 1, false, true>(ta, grid, st);
+  if (ta.g.offsets == nullptr) {
+    if constexpr (PFX == 1) {
+      if (ta.sp_tiles == 0) return launch_pfx_t<GATED, 1, false, true, false>(ta, grid, st);
+    }
+    return launch_pfx_t<GATED, PFX, true, false, false>(ta, grid, st);
   }
-  return launch_pfx_t<GATED, PFX, false, false>(ta, grid, st);
+  // (with the shared experts' tiles in the same launch the two-problem
+  // kernel keeps whole tiles: its tail variant needs more registers than
+  // two waves per SIMD allow)
+  if (ta.sp_tiles > 0) return launch_pfx_t<GATED, PFX, true, false, false>(ta, grid, st);
+  return launch_pfx_t<GATED, PFX, false, false, true>(ta, grid, st);
 }
 
 // Host-side checks of one problem: no blocked layouts, at most kMaxGroups
@@ -553,8 +769,10 @@ hipError_t launch_pfx(const TiledArgs& ta, long long grid, hipStream_t st) {
 // rows.
 bool tiled_ok(const Segments& seg, const GemmArgs& a) {
   if (seg.groups > kMaxGroups || a.x_blocked || a.out_blocked) return false;
+  // grouped problems: tail tiles read 2 kBN weight rows, and only a single K segment
+  if (a.static_rows == 0 && a.kseg < a.K) return false;
   const size_t x_span = static_cast<size_t>(a.x_row_count > 0 ? a.x_row_count : kBM) * a.K * 2;
-  const size_t w_span = (static_cast<size_t>(kBN) * a.ldw +
+  const size_t w_span = (static_cast<size_t>(2 * kBN) * a.ldw +
                          (a.kseg < a.K ? static_cast<size_t>((a.K - 1) / a.kseg) * a.seg_stride : 0) + a.K) * 2;
   const size_t o_span = static_cast<size_t>(kBM + 1) * a.N * 2;
   return x_span < 0x80000000ull && w_span < 0x80000000ull && o_span < 0x80000000ull;
