@@ -18,13 +18,29 @@ struct RouteGating {
   float scale;
   int n_group, topk_group;
 };
+// The dispatch outputs of launch_permute (offsets, perm_token, inv_pos) for
+// the local slots of local_experts (nullptr: slot = expert id).
+struct DispatchArgs {
+  const int32_t* local_experts;
+  int E_local;
+  int32_t* offsets;
+  int32_t* perm_token;
+  int32_t* inv_pos;
+};
+// Batches of at most this many (token, expert) pairs are dispatched by one block.
+constexpr int kDispatchPairs = 512;
+
 // Top-k selection + gates; when counts != nullptr also accumulates the
 // source x expert counts (and sets expert_load if non-null, which must have
 // been zeroed on the stream before).  gating == nullptr: softmax over the
-// picks, unscaled, no group limit.
+// picks, unscaled, no group limit.  dispatch (nullable): when the batch is
+// small enough for one block to route it (decode-sized batches), that block
+// also writes the dispatch, exactly as launch_permute would; *dispatched
+// says whether it did (the caller then skips launch_permute).
 hipError_t launch_route(int T, int E, int k, const float* logits, int32_t* topk_idx,
                         float* topk_w, const int32_t* src, int S, int64_t* counts,
-                        int32_t* expert_load, const RouteGating* gating, hipStream_t st);
+                        int32_t* expert_load, const RouteGating* gating, hipStream_t st,
+                        const DispatchArgs* dispatch = nullptr, bool* dispatched = nullptr);
 // Counts from (src, topk_idx); expert_load as above.
 hipError_t launch_route_stats(int T, int k, int S, int E, const int32_t* src,
                               const int32_t* topk_idx, int64_t* counts, int32_t* expert_load,

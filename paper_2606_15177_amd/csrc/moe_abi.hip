@@ -412,15 +412,20 @@ int moe_forward(const moe_dims* d, const moe_gating* gating, const float* logits
     e = moe::launch_fill_i32(expert_load, d->E, 0, st);
     if (e != hipSuccess) return MOE_ERR_DEVICE;
   }
+  // decode-sized batches: the routing launch also writes the dispatch
+  const moe::DispatchArgs disp{local_experts, d->E_local, offsets, perm_token, inv_pos};
+  bool dispatched = false;
   e = moe::launch_route(d->T, d->E, d->k, logits, topk_idx, topk_w, counts ? src : nullptr, d->S,
-                        counts, counts ? expert_load : nullptr, &rg, st);
+                        counts, counts ? expert_load : nullptr, &rg, st, &disp, &dispatched);
   if (e != hipSuccess) return MOE_ERR_DEVICE;
   record(taps, 2 * MOE_STAGE_ROUTE + 1, st);
 
   record(taps, 2 * MOE_STAGE_PERMUTE, st);
-  e = moe::launch_permute(d->T, d->k, d->E, d->E_local, local_experts, topk_idx, offsets,
-                          perm_token, inv_pos, fw.permute_ws, st);
-  if (e != hipSuccess) return MOE_ERR_DEVICE;
+  if (!dispatched) {
+    e = moe::launch_permute(d->T, d->k, d->E, d->E_local, local_experts, topk_idx, offsets,
+                            perm_token, inv_pos, fw.permute_ws, st);
+    if (e != hipSuccess) return MOE_ERR_DEVICE;
+  }
   // no gathered copy of x: the gate/up GEMM reads its rows through perm_token
   record(taps, 2 * MOE_STAGE_PERMUTE + 1, st);
 

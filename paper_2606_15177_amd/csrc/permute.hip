@@ -17,65 +17,13 @@
 // kernel does the three steps.  The row gather x_perm[r] = x[perm_token[r]]
 // is a separate, bandwidth-bound kernel that copies 16-byte vectors.
 #include "common.h"
+#include "dispatch_impl.h"
 #include "kernels.h"
 
 namespace moe {
 namespace {
 
-constexpr int kTile = 512;
-
-// slot_of[e] = local slot hosting expert e, or -1.  An expert listed twice
-// (outside the documented contract) resolves to its lowest slot, the same in
-// every kernel, so the count and scatter passes always agree.  Ends with a
-// barrier.
-__device__ void build_slot_map(int* slot_of, int E, int E_local, const int32_t* local_experts) {
-  if (local_experts == nullptr) {
-    for (int e = threadIdx.x; e < E; e += blockDim.x) slot_of[e] = e;
-  } else {
-    for (int e = threadIdx.x; e < E; e += blockDim.x) slot_of[e] = E_local;
-    __syncthreads();
-    for (int s = threadIdx.x; s < E_local; s += blockDim.x) {
-      const int e = local_experts[s];
-      if (e >= 0 && e < E) atomicMin(&slot_of[e], s);
-    }
-    __syncthreads();
-    for (int e = threadIdx.x; e < E; e += blockDim.x)
-      if (slot_of[e] >= E_local) slot_of[e] = -1;
-  }
-  __syncthreads();
-}
-
-__device__ __forceinline__ int slot_lookup(const int* slot_of, int e, int E) {
-  return (e >= 0 && e < E) ? slot_of[e] : -1;
-}
-
-// Pairs of one slot inside a 64-pair chunk, ranked by ballot + popcount
-__device__ __forceinline__ void scatter_chunk(int p, int n_pairs, int k, int E, const int* slot_of,
-                                              int* next, const int32_t* __restrict__ topk_idx,
-                                              int32_t* __restrict__ perm_token,
-                                              int32_t* __restrict__ inv_pos) {
-  const int lane = lane_id();
-  const uint64_t below = (1ull << lane) - 1ull;
-  int s = -1;
-  if (p < n_pairs) {
-    s = slot_lookup(slot_of, topk_idx[p], E);
-    if (s < 0) inv_pos[p] = -1;
-  }
-  uint64_t pending = __ballot(s >= 0);
-  while (pending) {
-    const int leader = __ffsll(static_cast<long long>(pending)) - 1;
-    const int sl = __shfl(s, leader);
-    const uint64_t same = __ballot(s == sl);
-    const int base = next[sl];
-    if (s == sl) {
-      const int pos = base + __popcll(same & below);
-      perm_token[pos] = p / k;
-      inv_pos[p] = pos;
-    }
-    if (lane == leader) next[sl] = base + __popcll(same);
-    pending &= ~same;
-  }
-}
+constexpr int kTile = kDispatchPairs;  // pairs per tile of the count and scatter passes
 
 __global__ __launch_bounds__(256) void perm_count_kernel(int n_pairs, int E, int E_local,
                                                          const int32_t* __restrict__ local_experts,
@@ -97,37 +45,6 @@ __global__ __launch_bounds__(256) void perm_count_kernel(int n_pairs, int E, int
     tile_counts[static_cast<size_t>(blockIdx.x) * E_local + s] = cnt[s];
 }
 
-// Exclusive scan of one value per thread over a block of blockDim.x threads
-// (a multiple of 64, at most 1024).  Returns the exclusive prefix; *total
-// receives the block sum.  Ends with a barrier.
-__device__ int block_exclusive_scan(int v, int* total) {
-  __shared__ int wsum[16];
-  const int lane = lane_id();
-  const int wave = threadIdx.x / kWave;
-  int inc = v;
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const int o = __shfl_up(inc, off);
-    if (lane >= off) inc += o;
-  }
-  if (lane == kWave - 1) wsum[wave] = inc;
-  __syncthreads();
-  if (wave == 0) {
-    const int n_waves = blockDim.x / kWave;
-    int w = lane < n_waves ? wsum[lane] : 0;
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) {
-      const int o = __shfl_up(w, off);
-      if (lane >= off) w += o;
-    }
-    if (lane < n_waves) wsum[lane] = w;  // inclusive over waves
-  }
-  __syncthreads();
-  const int before = wave > 0 ? wsum[wave - 1] : 0;
-  *total = wsum[blockDim.x / kWave - 1];
-  __syncthreads();
-  return before + inc - v;
-}
 
 __global__ __launch_bounds__(256) void perm_scan_kernel(int n_tiles, int E_local,
                                                         int32_t* __restrict__ tile_counts,
@@ -217,27 +134,7 @@ __global__ __launch_bounds__(1024) void perm_single_kernel(int n_pairs, int k, i
                                                            int32_t* __restrict__ perm_token,
                                                            int32_t* __restrict__ inv_pos) {
   extern __shared__ int sm[];
-  int* slot_of = sm;
-  int* cnt = sm + E;  // per-slot count, then next free row
-  for (int s = threadIdx.x; s < E_local; s += blockDim.x) cnt[s] = 0;
-  build_slot_map(slot_of, E, E_local, local_experts);
-  for (int p = threadIdx.x; p < n_pairs; p += blockDim.x) {
-    const int s = slot_lookup(slot_of, topk_idx[p], E);
-    if (s >= 0) atomicAdd(&cnt[s], 1);
-  }
-  __syncthreads();
-  const int own = threadIdx.x < E_local ? cnt[threadIdx.x] : 0;
-  int total;
-  const int excl = block_exclusive_scan(own, &total);
-  if (threadIdx.x < E_local) {
-    offsets[threadIdx.x] = excl;
-    cnt[threadIdx.x] = excl;
-  }
-  if (threadIdx.x == 0) offsets[E_local] = total;
-  __syncthreads();
-  if (threadIdx.x < kWave)
-    for (int c0 = 0; c0 < n_pairs; c0 += kWave)
-      scatter_chunk(c0 + threadIdx.x, n_pairs, k, E, slot_of, cnt, topk_idx, perm_token, inv_pos);
+  dispatch_one_block(n_pairs, k, E, E_local, local_experts, topk_idx, offsets, perm_token, inv_pos, sm);
 }
 
 __global__ __launch_bounds__(256) void gather_rows_kernel(int H, const int32_t* __restrict__ perm_token,

@@ -19,11 +19,16 @@
 // over those sums keep groups, and the experts of the other groups drop out of
 // the selection (key 0, below every kept expert, NaN included).
 //
+// Decode-sized batches (at most 512 pairs, four token groups): one block
+// routes the whole batch and then writes its dispatch (offsets, perm_token,
+// inv_pos) as the permute kernels would, saving a launch.
+//
 // Statistics (Sec. 5.1, the matrices A_{l,s,e} and B_{l,e}): each block
 // counts its pairs into an S x E int32 histogram in LDS and flushes the
 // non-zero bins with one 64-bit atomic add each.  Integer atomics make the
 // result independent of the order in which blocks land.
 #include "common.h"
+#include "dispatch_impl.h"
 #include "kernels.h"
 
 namespace moe {
@@ -84,6 +89,9 @@ struct RouteKernelArgs {
   const float* bias;     // [E] selection-only bias (gate 2), nullable
   float scale;           // gates are multiplied by this
   int n_group, topk_group;  // group limit when n_group > 1
+  // the dispatch in the same launch (one block routes the whole batch)
+  bool disp;
+  DispatchArgs d;
 };
 
 __device__ __forceinline__ float sigmoid_score(float l) {
@@ -275,6 +283,13 @@ __global__ __launch_bounds__(kBlock) void route_kernel(RouteKernelArgs a) {
     __syncthreads();
     flush_hist(hist, a.lds_bins, E, a.counts, a.expert_load);
   }
+  if (a.disp) {
+    // this block routed the whole batch: its expert ids are in topk_idx
+    __syncthreads();
+    int* sm = hist + a.lds_bins + (grouped ? kGroups * E : 0);
+    dispatch_one_block(T * k, k, E, a.d.E_local, a.d.local_experts, a.topk_idx, a.d.offsets, a.d.perm_token,
+                       a.d.inv_pos, sm);
+  }
 }
 
 __global__ __launch_bounds__(kBlock) void stats_kernel(int n_pairs, int k, int S, int E,
@@ -306,34 +321,41 @@ __global__ void fill_i32_kernel(int32_t* p, int n, int32_t value) {
 }
 
 template <int G, int V, bool EXT>
-hipError_t launch_route_gv(const RouteKernelArgs& in, hipStream_t st) {
+hipError_t launch_route_gv(const RouteKernelArgs& in, hipStream_t st, bool* dispatched) {
   constexpr int kGroups = kBlock / G;
   RouteKernelArgs a = in;
   // One token per group and block: the selection is a chain of dependent
-  // lane reductions, so many resident blocks hide its latency.
+  // lane reductions, so many resident blocks hide its latency.  A batch
+  // whose dispatch fits one block (at most kDispatchPairs pairs, four token
+  // groups) is routed by a single block that then also dispatches it,
+  // which saves a launch for decode-sized batches.
   a.tokens_per_block = kGroups;
-  const int blocks = ceil_div(a.T, a.tokens_per_block);
+  if (a.disp && (static_cast<long long>(a.T) * a.k > kDispatchPairs || a.T > 4 * kGroups || a.d.E_local > kBlock))
+    a.disp = false;
+  if (a.disp) a.tokens_per_block = a.T;
   a.lds_bins = (a.counts && a.S * a.E <= kLdsBinsMax) ? a.S * a.E : 0;
-  const size_t lds = a.lds_bins * sizeof(int) + ((EXT && a.n_group > 1) ? sizeof(float) * kGroups * a.E : 0);
-  if (EXT) {
-    static unsigned long long lds_set = 0;  // devices with the LDS limit raised
-    const hipError_t e_lds =
-        set_max_dynamic_lds(reinterpret_cast<const void*>(&route_kernel<G, V, EXT>),
-                            160 * 1024, &lds_set);
-    if (e_lds != hipSuccess) return e_lds;
-  }
+  const int blocks = ceil_div(a.T, a.tokens_per_block);
+  // histogram (at most 64 KB), group-limit staging (EXT), dispatch tables;
+  // the block-scan's partial sums take 64 more bytes of static LDS
+  const size_t lds = a.lds_bins * sizeof(int) + ((EXT && a.n_group > 1) ? sizeof(float) * kGroups * a.E : 0) +
+                     (a.disp ? sizeof(int) * (a.E + a.d.E_local) : 0);
+  if (dispatched) *dispatched = a.disp;
+  static unsigned long long lds_set = 0;  // devices with the LDS limit raised
+  const hipError_t e_lds =
+      set_max_dynamic_lds(reinterpret_cast<const void*>(&route_kernel<G, V, EXT>), 160 * 1024 - 1024, &lds_set);
+  if (e_lds != hipSuccess) return e_lds;
   hipLaunchKernelGGL((route_kernel<G, V, EXT>), dim3(blocks), dim3(kBlock), lds, st, a);
   return hipGetLastError();
 }
 
 template <int G, bool EXT>
-hipError_t launch_route_g(const RouteKernelArgs& a, int V, hipStream_t st) {
+hipError_t launch_route_g(const RouteKernelArgs& a, int V, hipStream_t st, bool* dispatched) {
   switch (V) {
-    case 1: return launch_route_gv<G, 1, EXT>(a, st);
-    case 2: return launch_route_gv<G, 2, EXT>(a, st);
-    case 4: return launch_route_gv<G, 4, EXT>(a, st);
-    case 8: return launch_route_gv<G, 8, EXT>(a, st);
-    default: return launch_route_gv<G, 16, EXT>(a, st);
+    case 1: return launch_route_gv<G, 1, EXT>(a, st, dispatched);
+    case 2: return launch_route_gv<G, 2, EXT>(a, st, dispatched);
+    case 4: return launch_route_gv<G, 4, EXT>(a, st, dispatched);
+    case 8: return launch_route_gv<G, 8, EXT>(a, st, dispatched);
+    default: return launch_route_gv<G, 16, EXT>(a, st, dispatched);
   }
 }
 
@@ -343,7 +365,7 @@ hipError_t launch_route_g(const RouteKernelArgs& a, int V, hipStream_t st) {
 // Narrow groups route more tokens per wave, and a max over 16 lanes is four
 // DPP steps within a row.
 template <bool EXT>
-hipError_t launch_route_ext(const RouteKernelArgs& a, hipStream_t st) {
+hipError_t launch_route_ext(const RouteKernelArgs& a, hipStream_t st, bool* dispatched) {
   const int E = a.E;
   const int need = max(a.k, EXT && a.n_group > 1 ? a.n_group : 1);
   int G = 2;
@@ -356,12 +378,12 @@ hipError_t launch_route_ext(const RouteKernelArgs& a, hipStream_t st) {
   int V = 1;
   while (V * G < E) V *= 2;
   switch (G) {
-    case 2: return launch_route_g<2, EXT>(a, V, st);
-    case 4: return launch_route_g<4, EXT>(a, V, st);
-    case 8: return launch_route_g<8, EXT>(a, V, st);
-    case 16: return launch_route_g<16, EXT>(a, V, st);
-    case 32: return launch_route_g<32, EXT>(a, V, st);
-    default: return launch_route_g<64, EXT>(a, V, st);
+    case 2: return launch_route_g<2, EXT>(a, V, st, dispatched);
+    case 4: return launch_route_g<4, EXT>(a, V, st, dispatched);
+    case 8: return launch_route_g<8, EXT>(a, V, st, dispatched);
+    case 16: return launch_route_g<16, EXT>(a, V, st, dispatched);
+    case 32: return launch_route_g<32, EXT>(a, V, st, dispatched);
+    default: return launch_route_g<64, EXT>(a, V, st, dispatched);
   }
 }
 
@@ -369,9 +391,15 @@ hipError_t launch_route_ext(const RouteKernelArgs& a, hipStream_t st) {
 
 hipError_t launch_route(int T, int E, int k, const float* logits, int32_t* topk_idx,
                         float* topk_w, const int32_t* src, int S, int64_t* counts,
-                        int32_t* expert_load, const RouteGating* gating, hipStream_t st) {
+                        int32_t* expert_load, const RouteGating* gating, hipStream_t st,
+                        const DispatchArgs* dispatch, bool* dispatched) {
+  if (dispatched) *dispatched = false;
   if (T == 0) return hipSuccess;
   RouteKernelArgs a{};
+  if (dispatch) {
+    a.disp = true;
+    a.d = *dispatch;
+  }
   a.T = T;
   a.E = E;
   a.k = k;
@@ -391,7 +419,7 @@ hipError_t launch_route(int T, int E, int k, const float* logits, int32_t* topk_
     a.n_group = gating->n_group;
     a.topk_group = gating->topk_group;
   }
-  return ext ? launch_route_ext<true>(a, st) : launch_route_ext<false>(a, st);
+  return ext ? launch_route_ext<true>(a, st, dispatched) : launch_route_ext<false>(a, st, dispatched);
 }
 
 hipError_t launch_route_stats(int T, int k, int S, int E, const int32_t* src,

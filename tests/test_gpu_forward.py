@@ -79,6 +79,11 @@ def test_forward_tiny_all_tokens_and_determinism(moe):
     dict(T=63, H=136, I=200, n_shared=2, I_shared=72), dict(T=300, H=200, I=136, E=12, k=3, E_local=12),
     dict(T=777, E=33, k=5, E_local=7, local_layout="choice", n_shared=1, I_shared=64),
     dict(T=100, src_layout="blocks"), dict(T=100, src_layout="interleaved", S=3),
+    # routing and dispatch in one launch (at most 512 pairs and four token
+    # groups of the routing block) and just past its limits
+    dict(T=128, k=4), dict(T=129, k=2), dict(T=128, E=8, k=5),
+    dict(T=32, E=256, k=8, E_local=32, local_layout="choice", S=8),
+    dict(T=16, E=1024, k=8, E_local=300, local_layout="choice", S=16),   # a 64 KB statistics histogram too
 ])
 def test_forward_variants(moe, variant):
     cfg = W.CONFIGS["tiny"].replace(name="variant", **variant)
