@@ -126,8 +126,8 @@ def stage_work(cfg, R: int, active: int) -> dict:
 
 # The sources of the layer's kernels: a profile's counters stay valid while
 # these are unchanged (placement and diagnostics kernels do not run in a step).
-LAYER_SOURCES = ("common.h", "ffn_impl.h", "route.hip", "permute.hip", "ffn_skinny.hip", "ffn_tiled.hip",
-                 "combine.hip")
+LAYER_SOURCES = ("common.h", "ffn_impl.h", "dispatch_impl.h", "route.hip", "permute.hip", "ffn_skinny.hip",
+                 "ffn_tiled.hip", "combine.hip")
 
 
 def source_digest(names=LAYER_SOURCES) -> str:

@@ -56,8 +56,10 @@
 //
 // Epilogue.  A lane holds row r, columns 8*v + 4*h + 0..3 (v < 4, h = lane
 // half) of each 32 x 32 accumulator tile.  Values are converted in bf16
-// pairs and a swap between the lane halves (v_permlane32_swap) gives every
-// lane 8 consecutive columns, written as one 16-byte store.
+// pairs; the down projection stages them through 4 KB of LDS per wave (free
+// during the epilogue) so that each 16-byte store instruction writes eight
+// whole 128-byte lines, the gated projection stores them directly after a
+// swap between the lane halves.
 #include "ffn_impl.h"
 
 namespace moe {
@@ -360,48 +362,90 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   };
   // the wave's output columns: WCOLS of them from col_w; rows from xr0
   constexpr int WCOLS = GATED ? 64 : 128;
-  auto epilogue = [&](const TileInfo& ti, int xr0, int col_w) {
+  // Epilogue.  The down projection's wave writes 128 columns per row: its
+  // outputs go through scr, 4 KB of LDS that only this wave touches until it
+  // issues its next loads, so that every store instruction writes eight
+  // whole 128-byte lines.  Per row group (32 rows) and pair of 32-column
+  // tiles the lanes write their converted values (row erow, columns
+  // 8 v4 + 4 ehalf .. +3 of each tile) into a block of 32 rows of 128 bytes,
+  // 16-byte chunk c of row r at slot c ^ (r & 7), then read it back by rows
+  // (lane L: chunk L % 8 of row 8 q + L / 8) and store.  The gated
+  // projection's wave writes half as many columns from twice the
+  // accumulators; there a swap between the lane halves gives each lane 8
+  // consecutive columns and the stores go straight out (measured faster than
+  // staging for it).
+  auto epilogue = [&](const TileInfo& ti, int xr0, int col_w, unsigned char* scr) {
     const GemmArgs& pr = prob(ti.p);
     const int ln = opaque_lane_id();
     const int erow = ln & 31, ehalf = ln >> 5;
     // The tile's output rows through a buffer descriptor: rows past the
     // group and columns past N get offsets >= 2^31, which the hardware
-    // drops, so the stores need no branches and the conversions of all of
-    // a row group's tiles can overlap.
+    // drops, so the stores need no branches.
     const __amdgpu_buffer_rsrc_t rs_o = __builtin_amdgcn_make_buffer_rsrc(
         pr.out + static_cast<size_t>(ti.row_base + ti.m0) * pr.N, 0, kRecords, kRsrcWord3);
+    // pk[2 v4 + h]: columns 8 v4 + 4 ehalf + 2 h, +1 of accumulator tile (tn, tm)
+    auto convert = [&](int tn, int tm, uint32_t (&pk)[8]) {
+#pragma unroll
+      for (int v4 = 0; v4 < 4; ++v4) {
+        float o[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float c0 = acc[tn][tm][4 * v4 + i];
+          if constexpr (GATED)
+            o[i] = silu(c0) * acc[tn + 2][tm][4 * v4 + i];
+          else
+            o[i] = c0;
+        }
+        pk[2 * v4] = cvt_pk_bf16(o[0], o[1]);
+        pk[2 * v4 + 1] = cvt_pk_bf16(o[2], o[3]);
+      }
+    };
 #pragma unroll
     for (int tm = 0; tm < 2; ++tm) {
-      const int r = xr0 + tm * 32 + erow;  // row within the tile
-      const uint32_t row_off = ti.m0 + r < ti.m ? static_cast<uint32_t>(r * pr.N * 2) : kInvalid;
-      constexpr int TOUT = GATED ? 2 : 4;
+      if constexpr (GATED) {
+        const int r = xr0 + tm * 32 + erow;  // row within the tile
+        const uint32_t row_off = ti.m0 + r < ti.m ? static_cast<uint32_t>(r * pr.N * 2) : kInvalid;
 #pragma unroll
-      for (int tn = 0; tn < TOUT; ++tn) {
-        uint32_t pk[8];  // pk[2*v4 + h]: columns 8*v4 + 4*ehalf + 2h, +1
+        for (int tn = 0; tn < 2; ++tn) {
+          uint32_t pk[8];
+          convert(tn, tm, pk);
 #pragma unroll
-        for (int v4 = 0; v4 < 4; ++v4) {
-          float o[4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float c0 = acc[tn][tm][4 * v4 + i];
-            if constexpr (GATED)
-              o[i] = silu(c0) * acc[tn + 2][tm][4 * v4 + i];
-            else
-              o[i] = c0;
+          for (int q = 0; q < 2; ++q) {  // columns 16q .. 16q+15 of the 32-column tile
+            // lower lanes keep columns 16q+0..3 and take 16q+4..7 from the
+            // upper half; upper lanes take 16q+8..11 and keep 16q+12..15
+            const auto s0 = __builtin_amdgcn_permlane32_swap(pk[4 * q], pk[4 * q + 2], false, false);
+            const auto s1 = __builtin_amdgcn_permlane32_swap(pk[4 * q + 1], pk[4 * q + 3], false, false);
+            const u32x4 v = {s0[0], s1[0], s0[1], s1[1]};
+            const int col = col_w + tn * 32 + 16 * q + 8 * ehalf;
+            const uint32_t off = col < pr.N ? row_off + static_cast<uint32_t>(col * 2) : kInvalid;
+            __builtin_amdgcn_raw_buffer_store_b128(v, rs_o, off | (row_off & kInvalid), 0, 0);
           }
-          pk[2 * v4] = cvt_pk_bf16(o[0], o[1]);
-          pk[2 * v4 + 1] = cvt_pk_bf16(o[2], o[3]);
         }
+      } else {
 #pragma unroll
-        for (int q = 0; q < 2; ++q) {  // columns 16q .. 16q+15 of the 32-column tile
-          // lower lanes keep columns 16q+0..3 and take 16q+4..7 from the upper
-          // half; upper lanes take 16q+8..11 and keep 16q+12..15
-          const auto s0 = __builtin_amdgcn_permlane32_swap(pk[4 * q], pk[4 * q + 2], false, false);
-          const auto s1 = __builtin_amdgcn_permlane32_swap(pk[4 * q + 1], pk[4 * q + 3], false, false);
-          const u32x4 v = {s0[0], s1[0], s0[1], s1[1]};
-          const int col = col_w + tn * 32 + 16 * q + 8 * ehalf;
-          const uint32_t off = col < pr.N ? row_off + static_cast<uint32_t>(col * 2) : kInvalid;
-          __builtin_amdgcn_raw_buffer_store_b128(v, rs_o, off | (row_off & kInvalid), 0, 0);
+        for (int tp = 0; tp < 2; ++tp) {
+#pragma unroll
+          for (int a2 = 0; a2 < 2; ++a2) {
+            uint32_t pk[8];
+            convert(2 * tp + a2, tm, pk);
+#pragma unroll
+            for (int v4 = 0; v4 < 4; ++v4) {
+              const int chunk = 4 * a2 + v4;  // columns 32 a2 + 8 v4 .. of the pair
+              typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+              *reinterpret_cast<u32x2*>(scr + erow * 128 + ((chunk ^ (erow & 7)) << 4) + 8 * ehalf) =
+                  u32x2{pk[2 * v4], pk[2 * v4 + 1]};
+            }
+          }
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int rr = 8 * q + (ln >> 3), c = ln & 7;
+            const u32x4 v = *reinterpret_cast<const u32x4*>(scr + rr * 128 + ((c ^ (rr & 7)) << 4));
+            const int r = xr0 + tm * 32 + rr;  // row within the tile
+            const int col = col_w + tp * 64 + 8 * c;
+            const uint32_t off =
+                (ti.m0 + r < ti.m && col < pr.N) ? static_cast<uint32_t>(r * pr.N * 2 + col * 2) : kInvalid;
+            __builtin_amdgcn_raw_buffer_store_b128(v, rs_o, off, 0, 0);
+          }
         }
       }
       __builtin_amdgcn_sched_barrier(0);
@@ -568,7 +612,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         mfma_set((C::KSTEPS - 1) & 1);
         __builtin_amdgcn_sched_barrier(0);
       }
-      epilogue(cur, xrow0, cur.nt * OUT_COLS + wn * WCOLS);
+      // the W part of the tile's last stage is free until this wave loads X
+      // of the stage three ahead into its own 4 KB of it
+      epilogue(cur, xrow0, cur.nt * OUT_COLS + wn * WCOLS, part_ptr(2 * (j - 1) + 1) + wave * 4096);
       zero_acc();
     }
   };
@@ -688,7 +734,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         __builtin_amdgcn_s_waitcnt(kWaitAll);  // own stage j+1 landed, LDS reads done
         phase_barrier();
       }
-      epilogue(cur, xrow0_t, cur.nt * OUT_COLS_T + wn_t * WCOLS);
+      // the buffer of the tile's last stage is free until the next loads
+      // into it; this wave's own W rows there are its 8 KB
+      epilogue(cur, xrow0_t, cur.nt * OUT_COLS_T + wn_t * WCOLS, t_buf((j - 1) & 1) + T_XPART + wave * (64 * C::ROW));
       zero_acc();
     }
   };
