@@ -130,6 +130,16 @@ __device__ __forceinline__ int wave_min(int v) {
   return v;
 }
 
+// An element of an index array that the kernel only reads, at a uniform
+// index, through the constant address space: a scalar load.  Its wait
+// (lgkmcnt) leaves the vector-memory counter alone; a vector load here would
+// be waited for with that counter, which completes in order, and so drain
+// every tile load and output store in flight.
+typedef const int __attribute__((address_space(4)))* ConstIntPtr;
+__device__ __forceinline__ int load_uniform(const int* p, int i) {
+  return ((ConstIntPtr)(uintptr_t)p)[i];
+}
+
 // Two GEMMs of one kind in one launch: the tiles of sp (static rows, e.g. the
 // shared experts over every token; sp_tiles of them, 0 when absent) come
 // first, then those of g (the routed experts).  One grid keeps every CU busy
@@ -258,8 +268,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       hi = wave_min(hi);
       const int g = __builtin_amdgcn_readfirstlane(cnt);
       ti.g = g;
-      ti.row_base = a.offsets[g];
-      ti.m = a.offsets[g + 1] - ti.row_base;
+      ti.row_base = load_uniform(a.offsets, g);
+      ti.m = load_uniform(a.offsets, g + 1) - ti.row_base;
       base = __builtin_amdgcn_readfirstlane(lo) * scale;
       mg = __builtin_amdgcn_readfirstlane(hi) - __builtin_amdgcn_readfirstlane(lo);
       if constexpr (TAIL) {
@@ -467,9 +477,25 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     int x_p = 1, w_p = 1, x_nkb = 1, w_nkb = 1;  // each stream's problem and its K stages
     uint32_t kx0 = 0, kx1 = 0, kw0 = 0, kw1 = 0;
 
-    auto x_setup = [&](int t_in) {
+    // The gathered source rows (x_rows) of the X stream's next tile are
+    // loaded one tile ahead, so that waiting for them never waits for the
+    // tile loads in flight (the vector-memory counter completes in order).
+    int xr_next[C::LPP];
+    auto x_rows_of = [&](int t, int (&xr)[C::LPP]) {
+      const TileInfo ti = tile_info(t);
+      const GemmArgs& q = prob(PAIR ? ti.p : 1);
+      const int ln = opaque_lane_id();
+      if (q.x_rows) {
+#pragma unroll
+        for (int i = 0; i < C::LPP; ++i) {
+          const int r = 32 * wave + C::RPI * i + ln / C::CPR;
+          xr[i] = q.x_rows[ti.row_base + (ti.m0 + r < ti.m ? ti.m0 + r : 0)];
+        }
+      }
+    };
+    // prefetched: xr_next holds the rows of t_in (loaded by the previous call)
+    auto x_setup = [&](int t_in, bool prefetched) {
       const bool live = t_in < run_end;
-      const uint32_t dead = live ? 0u : kInvalid;
       const int t = live ? t_in : run_start;
       const TileInfo ti = tile_info(t);
       x_p = PAIR ? ti.p : 1;
@@ -480,16 +506,19 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       rs_x = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(xb), 0, kRecords, kRsrcWord3);
       int xr[C::LPP];
 #pragma unroll
-      for (int i = 0; i < C::LPP; ++i) {
-        const int r = 32 * wave + C::RPI * i + ln / C::CPR;
-        xr[i] = r;
-        if (q.x_rows) xr[i] = q.x_rows[ti.row_base + (ti.m0 + r < ti.m ? ti.m0 + r : 0)];
+      for (int i = 0; i < C::LPP; ++i) xr[i] = 32 * wave + C::RPI * i + ln / C::CPR;
+      if (q.x_rows) {
+        if (live && !prefetched) x_rows_of(t, xr_next);
+#pragma unroll
+        for (int i = 0; i < C::LPP; ++i) xr[i] = xr_next[i];
       }
+      // past the run (dead) the loads carry invalid offsets: no traffic
 #pragma unroll
       for (int i = 0; i < C::LPP; ++i) {
         const int r = 32 * wave + C::RPI * i + ln / C::CPR;
-        xoff[i] = (ti.m0 + r < ti.m ? static_cast<uint32_t>(xr[i] * q.K * 2 + chunk_of(i, ln) * 16) : kInvalid) | dead;
+        xoff[i] = (live && ti.m0 + r < ti.m) ? static_cast<uint32_t>(xr[i] * q.K * 2 + chunk_of(i, ln) * 16) : kInvalid;
       }
+      if (t_in + static_cast<int>(gridDim.x) < run_end) x_rows_of(t_in + gridDim.x, xr_next);
     };
     auto w_setup = [&](int t_in) {
       const bool live = t_in < run_end;
@@ -539,7 +568,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       if (++x_kb == (PAIR ? x_nkb : nkb_g)) {
         x_kb = 0;
         x_tile += gridDim.x;
-        x_setup(x_tile);
+        x_setup(x_tile, true);
       }
       x_kstep();
     };
@@ -562,7 +591,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     zero_acc();
     x_tile = w_tile = run_start;
     x_kb = w_kb = 0;
-    x_setup(run_start);
+    x_setup(run_start, false);
     x_kstep();
     w_setup(run_start);
     w_kstep();
@@ -655,20 +684,32 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     uint32_t txoff[T_XL], twoff[T_WL];
     int tt = first, tkb = 0;
     uint32_t tk0 = 0, tk1 = 0;
-    auto t_setup = [&](int t_in) {
+    // gathered source rows one tile ahead, as for the full tiles
+    int txr_next[T_XL];
+    auto t_rows_of = [&](int t) {
+      const TileInfo ti = tile_info(t);
+      const int ln = opaque_lane_id();
+#pragma unroll
+      for (int i = 0; i < T_XL; ++i) {
+        const int r = 16 * wave + C::RPI * i + ln / C::CPR;
+        txr_next[i] = a.x_rows[ti.row_base + (ti.m0 + r < ti.m ? ti.m0 + r : 0)];
+      }
+    };
+    auto t_setup = [&](int t_in, bool prefetched) {
       const bool live = t_in < run_end;
       const uint32_t dead = live ? 0u : kInvalid;
       const TileInfo ti = tile_info(live ? t_in : run_start);
       const int ln = opaque_lane_id();
       const uint16_t* xb = a.x_rows ? a.x : a.x + static_cast<size_t>(ti.row_base + ti.m0) * a.K;
       trs_x = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(xb), 0, kRecords, kRsrcWord3);
+      if (a.x_rows && live && !prefetched) t_rows_of(t_in);
 #pragma unroll
       for (int i = 0; i < T_XL; ++i) {
         const int r = 16 * wave + C::RPI * i + ln / C::CPR;
-        const bool in = ti.m0 + r < ti.m;
-        const int xr = a.x_rows ? a.x_rows[ti.row_base + (in ? ti.m0 + r : 0)] : r;
-        txoff[i] = (in ? static_cast<uint32_t>(xr * a.K * 2 + chunk_of(i, ln) * 16) : kInvalid) | dead;
+        const int xr = a.x_rows ? txr_next[i] : r;
+        txoff[i] = (live && ti.m0 + r < ti.m) ? static_cast<uint32_t>(xr * a.K * 2 + chunk_of(i, ln) * 16) : kInvalid;
       }
+      if (a.x_rows && t_in + static_cast<int>(gridDim.x) < run_end) t_rows_of(t_in + gridDim.x);
       const int col0 = ti.nt * OUT_COLS_T;
       const size_t gofs = static_cast<size_t>(ti.g) * a.group_stride + static_cast<size_t>(col0) * a.ldw;
       const bool up = GATED && (wave & 1);  // W rows 64w .. 64w+63: gate rows for even w, up rows for odd w
@@ -691,7 +732,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       if (++tkb == nkb_g) {
         tkb = 0;
         tt += gridDim.x;
-        t_setup(tt);
+        t_setup(tt, true);
       }
       t_kstep();
     };
@@ -706,7 +747,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     zero_acc();
     tt = run_start;
     tkb = 0;
-    t_setup(tt);
+    t_setup(tt, false);
     t_kstep();
 #pragma unroll
     for (int i = 0; i < T_XL + T_WL; ++i) t_load(0, i);
