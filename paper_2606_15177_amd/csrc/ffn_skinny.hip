@@ -11,11 +11,12 @@
 // same 32 output columns; down: NB consecutive 32-row blocks), in steps of
 // KS elements, so every token fragment read from L2 feeds NB MFMAs.  A step
 // of a block (32 rows x KS) is loaded by buffer_load_dwordx4 ... lds straight
-// into the wave's own ring of DEPTH step buffers in LDS; one load instruction
+// into the wave's own ring of two step buffers in LDS; one load instruction
 // covers 64/(KS/8) whole rows of KS/8 16-byte pieces, so every request is a
 // full run of 128-byte lines.  Piece c of row r lands in slot c ^ (r mod KS/8),
-// which spreads the 32 rows of an MFMA fragment read over the banks.  DEPTH-1
-// steps stay in flight per wave without holding registers.  No workgroup
+// which spreads the 32 rows of an MFMA fragment read over the banks.  The
+// next step's weights stay in flight per wave without holding registers,
+// its token fragments in registers.  No workgroup
 // barrier is taken inside the K loop; one barrier at the end reduces the K
 // parts (fixed order, deterministic) and applies SwiGLU.  Each workgroup
 // starts its K walk at a rotated step so that concurrently running
@@ -34,7 +35,7 @@ __device__ __forceinline__ void stream_lds16(__amdgpu_buffer_rsrc_t rs, unsigned
 }
 
 template <bool GATED, int NB, int KP, int KS, int DEPTH>
-__global__ __launch_bounds__(KP* kWave) void skinny_kernel(GemmArgs a) {
+__global__ __launch_bounds__(KP* kWave) __attribute__((amdgpu_waves_per_eu(2, 2))) void skinny_kernel(GemmArgs a) {
   constexpr int ROWB = KS * 2;            // bytes of one row segment
   constexpr int PPR = KS / 8;             // 16-byte pieces per row segment
   constexpr int RPI = kWave / PPR;        // rows per load instruction
@@ -43,7 +44,8 @@ __global__ __launch_bounds__(KP* kWave) void skinny_kernel(GemmArgs a) {
   constexpr int STEPB = 32 * ROWB;        // bytes of one block step
   constexpr int WG_ROWS = GATED ? 32 : 32 * NB;  // output columns of the workgroup
   static_assert(RPI * PPR == kWave && NLD * RPI == 32 && RPI * ROWB == 1024, "step shape");
-  static_assert(DEPTH >= 2 && (!GATED || NB == 2), "ring depth / gated blocks");
+  // two-step rings: the waits below count the loads of exactly one step ahead
+  static_assert(DEPTH == 2 && (!GATED || NB == 2), "ring depth / gated blocks");
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
 
   const int g = blockIdx.y;
@@ -53,7 +55,7 @@ __global__ __launch_bounds__(KP* kWave) void skinny_kernel(GemmArgs a) {
     m = a.offsets[g + 1] - row_base;
   }
   if (m <= 0) return;  // an expert with no rows costs no weight traffic
-  const int wave = threadIdx.x / kWave, lane = lane_id();
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = lane_id();
   // first chunk of this group in the chunk-blocked layouts: the chunks of the
   // groups before it (every wave, lanes over groups)
   int chunk_base = 0;
@@ -109,12 +111,15 @@ __global__ __launch_bounds__(KP* kWave) void skinny_kernel(GemmArgs a) {
     unsigned char* dst = wl + (j % DEPTH) * (NB * STEPB);
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
+      // every load is issued (the wait counts rely on it): a piece past K
+      // gets an offset past the descriptor's range
       const int kk = kk0 + piece[i] * 8;
       const bool kok = kk < a.K;
-      const uint32_t col = kok ? static_cast<uint32_t>((segmented ? weight_col_offset(a, kk) : static_cast<size_t>(kk)) * 2) : 0u;
+      const int kc = kok ? kk : kk0;
+      const uint32_t col = static_cast<uint32_t>((segmented ? weight_col_offset(a, kc) : static_cast<size_t>(kc)) * 2);
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
-        const uint32_t off = kok ? roff[b][i] + col : kInvalidOff;
+        const uint32_t off = (roff[b][i] + col) | (kok ? 0u : kInvalidOff);
         if (GATED && b == 1)
           stream_lds16(rs1, dst + b * STEPB + i * 1024, off);
         else
@@ -147,39 +152,102 @@ __global__ __launch_bounds__(KP* kWave) void skinny_kernel(GemmArgs a) {
     f32x16 acc[NB][2];
 #pragma unroll
     for (int b = 0; b < NB; ++b) acc[b][0] = acc[b][1] = f32x16{};
-    for (int s = 0; s < DEPTH - 1; ++s)
-      if (s < nq) issue(s);
-    for (int j = 0; j < nq; ++j) {
-      const int kb = kstep(j);
-      u32x4 xt[2][KK];
-#pragma unroll
-      for (int c = 0; c < 2; ++c)
-#pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-          const int k = kb * KS + 16 * kk + 8 * (lane >> 5);
-          const u32x4 zero = {0u, 0u, 0u, 0u};
-          xt[c][kk] = (tok_ok[c] && k < a.K) ? load16(xrow[c] + (kb * (KS / 16) + kk) * kstride) : zero;
+    if constexpr (GATED) {
+      // The token fragments of step j + 1 (2 KK loads into the other of two
+      // register sets; always issued, a lane out of range reading its row's
+      // first piece) go out before the weights of step j + 1, so that both are
+      // in flight while step j computes.  Pieces out of range are zeroed after
+      // the wait.
+      u32x4 xs[2][2][KK];
+      auto x_ok = [&](int kb, int c, int kk) {
+        return tok_ok[c] && kb * KS + 16 * kk + 8 * (lane >> 5) < a.K;
+      };
+      auto load_x = [&](int j, u32x4 (&dst)[2][KK]) {
+        const int kb = kstep(j);
+  #pragma unroll
+        for (int c = 0; c < 2; ++c)
+  #pragma unroll
+          for (int kk = 0; kk < KK; ++kk)
+            dst[c][kk] = load16(xrow[c] + (x_ok(kb, c, kk) ? (kb * (KS / 16) + kk) * kstride : 0));
+      };
+      auto step = [&](int j, u32x4 (&cur)[2][KK], u32x4 (&nxt)[2][KK]) {
+        // the slot refilled is the one step j-1 read, whose fragments are in
+        // registers by now
+        if (j + 1 < nq) {
+          load_x(j + 1, nxt);
+          issue(j + 1);
+          constexpr int kYounger = 2 * KK + NB * NLD;  // step j + 1's loads may stay in flight
+          __builtin_amdgcn_s_waitcnt((kYounger & 15) | ((kYounger >> 4) << 14) | (7 << 4) | (15 << 8));
+        } else {
+          __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
         }
-      // keep DEPTH-1 steps in flight; the slot refilled is the one step j-1
-      // read, whose fragments are in registers by now
-      if (j + DEPTH - 1 < nq) {
-        issue(j + DEPTH - 1);
-        constexpr int kYounger = NB * NLD;  // the loads just issued may stay in flight
-        __builtin_amdgcn_s_waitcnt((kYounger & 15) | ((kYounger >> 4) << 14) | (7 << 4) | (15 << 8));
-      } else {
-        __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
+        const int kb = kstep(j);
+  #pragma unroll
+        for (int c = 0; c < 2; ++c)
+  #pragma unroll
+          for (int kk = 0; kk < KK; ++kk) {
+            const u32x4 zero = {0u, 0u, 0u, 0u};
+            if (!x_ok(kb, c, kk)) cur[c][kk] = zero;
+          }
+        const unsigned char* bsl = wl + (j % DEPTH) * (NB * STEPB);
+  #pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+          const int p = 2 * kk + (lane >> 5);
+          const int row = lane & 31;
+          const int slot = row * ROWB + ((p ^ (row & (PPR - 1))) << 4);
+  #pragma unroll
+          for (int b = 0; b < NB; ++b) {
+            const u32x4 wv = *reinterpret_cast<const u32x4*>(bsl + b * STEPB + slot);
+            acc[b][0] = mfma32x32x16(as_bf16x8(wv), as_bf16x8(cur[0][kk]), acc[b][0]);
+            if (nch > 1) acc[b][1] = mfma32x32x16(as_bf16x8(wv), as_bf16x8(cur[1][kk]), acc[b][1]);
+          }
+        }
+      };
+      if (nq > 0) {
+        load_x(0, xs[0]);
+        issue(0);
       }
-      const unsigned char* bsl = wl + (j % DEPTH) * (NB * STEPB);
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        const int p = 2 * kk + (lane >> 5);
-        const int row = lane & 31;
-        const int slot = row * ROWB + ((p ^ (row & (PPR - 1))) << 4);
-#pragma unroll
-        for (int b = 0; b < NB; ++b) {
-          const u32x4 wv = *reinterpret_cast<const u32x4*>(bsl + b * STEPB + slot);
-          acc[b][0] = mfma32x32x16(as_bf16x8(wv), as_bf16x8(xt[0][kk]), acc[b][0]);
-          if (nch > 1) acc[b][1] = mfma32x32x16(as_bf16x8(wv), as_bf16x8(xt[1][kk]), acc[b][1]);
+      for (int j = 0; j < nq; j += 2) {
+        step(j, xs[0], xs[1]);
+        if (j + 1 < nq) step(j + 1, xs[1], xs[0]);
+      }
+    } else {
+      // down: step j's token fragments just before the weights of step j + 1
+      // (measured faster here than one step ahead)
+      for (int s = 0; s < DEPTH - 1; ++s)
+        if (s < nq) issue(s);
+      for (int j = 0; j < nq; ++j) {
+        const int kb = kstep(j);
+        u32x4 xt[2][KK];
+  #pragma unroll
+        for (int c = 0; c < 2; ++c)
+  #pragma unroll
+          for (int kk = 0; kk < KK; ++kk) {
+            const int k = kb * KS + 16 * kk + 8 * (lane >> 5);
+            const u32x4 zero = {0u, 0u, 0u, 0u};
+            xt[c][kk] = (tok_ok[c] && k < a.K) ? load16(xrow[c] + (kb * (KS / 16) + kk) * kstride) : zero;
+          }
+        // keep DEPTH-1 steps in flight; the slot refilled is the one step j-1
+        // read, whose fragments are in registers by now
+        if (j + DEPTH - 1 < nq) {
+          issue(j + DEPTH - 1);
+          constexpr int kYounger = NB * NLD;  // the loads just issued may stay in flight
+          __builtin_amdgcn_s_waitcnt((kYounger & 15) | ((kYounger >> 4) << 14) | (7 << 4) | (15 << 8));
+        } else {
+          __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
+        }
+        const unsigned char* bsl = wl + (j % DEPTH) * (NB * STEPB);
+  #pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+          const int p = 2 * kk + (lane >> 5);
+          const int row = lane & 31;
+          const int slot = row * ROWB + ((p ^ (row & (PPR - 1))) << 4);
+  #pragma unroll
+          for (int b = 0; b < NB; ++b) {
+            const u32x4 wv = *reinterpret_cast<const u32x4*>(bsl + b * STEPB + slot);
+            acc[b][0] = mfma32x32x16(as_bf16x8(wv), as_bf16x8(xt[0][kk]), acc[b][0]);
+            if (nch > 1) acc[b][1] = mfma32x32x16(as_bf16x8(wv), as_bf16x8(xt[1][kk]), acc[b][1]);
+          }
         }
       }
     }
