@@ -336,6 +336,9 @@ bool skinny_ok(const GemmArgs& a) {
 hipError_t launch_skinny(const Segments& seg, const GemmArgs& a, bool gated, hipStream_t st) {
   // the blocked layouts are defined by the device-side offsets
   if ((a.x_blocked || a.out_blocked) && a.offsets == nullptr) return hipErrorInvalidValue;
+  // the gate/up kernel's out-of-range token lanes read their row's first
+  // piece, which exists only in the row layout
+  if (gated && a.x_blocked) return hipErrorInvalidValue;
   if (!skinny_ok(a)) return hipErrorInvalidValue;
   // gate/up: the gate and up blocks of 32 rows per wave; down: two 32-row
   // blocks per wave; 4 K parts, 64-wide steps, two-step rings (64 KB of LDS,
