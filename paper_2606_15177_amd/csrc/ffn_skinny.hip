@@ -162,13 +162,16 @@ __global__ __launch_bounds__(KP* kWave) __attribute__((amdgpu_waves_per_eu(2, 2)
       auto x_ok = [&](int kb, int c, int kk) {
         return tok_ok[c] && kb * KS + 16 * kk + 8 * (lane >> 5) < a.K;
       };
+      // chunk 1 only when the row block has a second chunk (uniform)
       auto load_x = [&](int j, u32x4 (&dst)[2][KK]) {
         const int kb = kstep(j);
-  #pragma unroll
-        for (int c = 0; c < 2; ++c)
-  #pragma unroll
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          if (c == 1 && nch < 2) break;
+#pragma unroll
           for (int kk = 0; kk < KK; ++kk)
             dst[c][kk] = load16(xrow[c] + (x_ok(kb, c, kk) ? (kb * (KS / 16) + kk) * kstride : 0));
+        }
       };
       auto step = [&](int j, u32x4 (&cur)[2][KK], u32x4 (&nxt)[2][KK]) {
         // the slot refilled is the one step j-1 read, whose fragments are in
@@ -176,26 +179,30 @@ __global__ __launch_bounds__(KP* kWave) __attribute__((amdgpu_waves_per_eu(2, 2)
         if (j + 1 < nq) {
           load_x(j + 1, nxt);
           issue(j + 1);
-          constexpr int kYounger = 2 * KK + NB * NLD;  // step j + 1's loads may stay in flight
-          __builtin_amdgcn_s_waitcnt((kYounger & 15) | ((kYounger >> 4) << 14) | (7 << 4) | (15 << 8));
+          // step j + 1's loads may stay in flight
+          constexpr int kYounger2 = 2 * KK + NB * NLD, kYounger1 = KK + NB * NLD;
+          if (nch > 1)
+            __builtin_amdgcn_s_waitcnt((kYounger2 & 15) | ((kYounger2 >> 4) << 14) | (7 << 4) | (15 << 8));
+          else
+            __builtin_amdgcn_s_waitcnt((kYounger1 & 15) | ((kYounger1 >> 4) << 14) | (7 << 4) | (15 << 8));
         } else {
           __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
         }
         const int kb = kstep(j);
-  #pragma unroll
+#pragma unroll
         for (int c = 0; c < 2; ++c)
-  #pragma unroll
+#pragma unroll
           for (int kk = 0; kk < KK; ++kk) {
             const u32x4 zero = {0u, 0u, 0u, 0u};
             if (!x_ok(kb, c, kk)) cur[c][kk] = zero;
           }
         const unsigned char* bsl = wl + (j % DEPTH) * (NB * STEPB);
-  #pragma unroll
+#pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
           const int p = 2 * kk + (lane >> 5);
           const int row = lane & 31;
           const int slot = row * ROWB + ((p ^ (row & (PPR - 1))) << 4);
-  #pragma unroll
+#pragma unroll
           for (int b = 0; b < NB; ++b) {
             const u32x4 wv = *reinterpret_cast<const u32x4*>(bsl + b * STEPB + slot);
             acc[b][0] = mfma32x32x16(as_bf16x8(wv), as_bf16x8(cur[0][kk]), acc[b][0]);
@@ -219,9 +226,9 @@ __global__ __launch_bounds__(KP* kWave) __attribute__((amdgpu_waves_per_eu(2, 2)
       for (int j = 0; j < nq; ++j) {
         const int kb = kstep(j);
         u32x4 xt[2][KK];
-  #pragma unroll
+#pragma unroll
         for (int c = 0; c < 2; ++c)
-  #pragma unroll
+#pragma unroll
           for (int kk = 0; kk < KK; ++kk) {
             const int k = kb * KS + 16 * kk + 8 * (lane >> 5);
             const u32x4 zero = {0u, 0u, 0u, 0u};
@@ -237,12 +244,12 @@ __global__ __launch_bounds__(KP* kWave) __attribute__((amdgpu_waves_per_eu(2, 2)
           __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
         }
         const unsigned char* bsl = wl + (j % DEPTH) * (NB * STEPB);
-  #pragma unroll
+#pragma unroll
         for (int kk = 0; kk < KK; ++kk) {
           const int p = 2 * kk + (lane >> 5);
           const int row = lane & 31;
           const int slot = row * ROWB + ((p ^ (row & (PPR - 1))) << 4);
-  #pragma unroll
+#pragma unroll
           for (int b = 0; b < NB; ++b) {
             const u32x4 wv = *reinterpret_cast<const u32x4*>(bsl + b * STEPB + slot);
             acc[b][0] = mfma32x32x16(as_bf16x8(wv), as_bf16x8(xt[0][kk]), acc[b][0]);
