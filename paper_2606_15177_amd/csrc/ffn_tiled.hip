@@ -16,9 +16,9 @@
 // device.
 //
 // Tail tiles.  An expert whose rows past its last whole m-tile number 1..128
-// takes them in tiles of 128 token rows x 512 weight rows, each covering two
-// column tiles, with their own LDS layout and pipeline (see TAIL): half the
-// tiles that a padded 256-row m-tile would take.
+// takes them in tiles of 128 token rows, with their own LDS layout and
+// pipeline (see TAIL): half the MFMA work per row of a padded 256-row
+// m-tile.
 //
 // Two problems.  The shared experts (static rows: every token) can run in
 // the routed experts' launch: their tiles come first, and each load stream
@@ -69,6 +69,7 @@ constexpr int kBM = 256;             // token rows per tile
 constexpr int kBN = 256;             // weight rows per tile
 constexpr int kThreads = 8 * kWave;  // eight waves, two per SIMD
 constexpr int kMaxGroups = 1024;
+constexpr int kHalfTailK = 4096;  // K from which grouped launches take half tail tiles
 constexpr int kBlockM = 8;           // m-tiles per block of a static group's tile order
 
 // One K stage and the ring of its parts.
@@ -140,6 +141,11 @@ __device__ __forceinline__ int load_uniform(const int* p, int i) {
   return ((ConstIntPtr)(uintptr_t)p)[i];
 }
 
+template <bool B>
+struct Half {
+  static constexpr bool value = B;
+};
+
 // Two GEMMs of one kind in one launch: the tiles of sp (static rows, e.g. the
 // shared experts over every token; sp_tiles of them, 0 when absent) come
 // first, then those of g (the routed experts).  One grid keeps every CU busy
@@ -158,16 +164,21 @@ struct TiledArgs {
 // whose token tiles would be fetched again for every n-tile.
 //
 // TAIL (grouped problems): a group whose rows past its last whole 256-row
-// m-tile number 1..128 runs them as tail tiles of 128 token rows x 512
-// weight rows (twice the columns of a full tile), half the tiles such a
-// padded last m-tile took.  Within a group the tiles go by pairs of
-// column tiles: the full tiles of column tiles 2p and 2p + 1 (m-tiles
-// fastest), then the tail tile that covers both, so the tail tile runs
-// beside the full tiles that read the same weight rows.  A tail tile has
-// its own LDS layout (two 80 KB stages: X [128 x 64], W [512 x 64]) and
-// pipeline; a workgroup drains its pipeline where its sequence of tiles
-// switches between the two kinds.
-template <bool GATED, int kPfx, bool PAIR, bool SBLK, bool TAIL>
+// m-tile number 1..128 runs them as tail tiles of 128 token rows, half the
+// MFMA work of a padded m-tile, in one of two shapes with their own LDS
+// layouts and pipelines.  A workgroup drains its pipeline where its sequence
+// of tiles switches between full and tail tiles.
+//  - TAIL 1, wide: 128 x 512 weight rows (two column tiles).  Within a group
+//    the tiles go by pairs of column tiles: the full tiles of column tiles 2p
+//    and 2p + 1 (m-tiles fastest), then the tail tile that covers both.
+//    Two 80 KB stages: X [128 x 64], W [512 x 64].
+//  - TAIL 2, half: 128 x 256 weight rows.  Within a group the tiles go by
+//    column tiles, m-tiles fastest, the tail tile last.  With half a full
+//    tile's work per stage it keeps pace with the full tiles that read the
+//    same weight rows and finds them in L2; a wide tail tile falls behind
+//    them on long K and reads its weights from HBM.  Three 48 KB stages:
+//    X [128 x 64], W [256 x 64].
+template <bool GATED, int kPfx, bool PAIR, bool SBLK, int TAIL>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void tiled_kernel(TiledArgs ta) {
   using C = Stage;
   const GemmArgs& a = ta.g;
@@ -186,7 +197,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   const int wm = wave & 3, wn = wave >> 2;
   const int lrow = lane & 31, lhalf = lane >> 5;
   const int n_tiles_n = ceil_div(a.N, OUT_COLS);
-  const int n_tiles_t = ceil_div(n_tiles_n, 2);  // column tiles of a tail tile (512 weight rows)
+  const int n_tiles_t = ceil_div(n_tiles_n, 2);  // column tiles of a wide tail tile (512 weight rows)
 
   // full m-tiles and tail tiles of a group of n rows
   auto group_shape = [&](int n, int& fm, int& tl) {
@@ -214,7 +225,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         if constexpr (TAIL) {
           int fm, tl;
           group_shape(n, fm, tl);
-          cnt = fm * n_tiles_n + tl * n_tiles_t;
+          cnt = TAIL == 1 ? fm * n_tiles_n + tl * n_tiles_t : (fm + tl) * n_tiles_n;
         } else {
           cnt = ceil_div(n, kBM);
         }
@@ -239,7 +250,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
 
   struct TileInfo {
     int p, g, row_base, m, m0, nt;  // p: 0 for sp, 1 for g
-    bool tail;                      // a tail tile (nt then counts 512-row column tiles)
+    bool tail;                      // a tail tile (wide tails: nt counts 512-row column tiles)
   };
   // group of tile t: the number of groups whose tiles all precede t
   auto tile_info = [&](int t_all) {
@@ -273,19 +284,30 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       base = __builtin_amdgcn_readfirstlane(lo) * scale;
       mg = __builtin_amdgcn_readfirstlane(hi) - __builtin_amdgcn_readfirstlane(lo);
       if constexpr (TAIL) {
-        // pairs of column tiles: the full tiles of columns 2p and 2p + 1
-        // (m-tiles fastest), then the tail tile of pair p
         int fm, tl;
         group_shape(ti.m, fm, tl);
         const int local = t - base;
-        const int per_pair = 2 * fm + tl;
-        const int pr = min(local / max(per_pair, 1), n_tiles_t - 1);
-        const int r = local - pr * per_pair;
-        const int nfull = min(2, n_tiles_n - 2 * pr) * fm;
-        const int fmd = max(fm, 1);
-        ti.tail = r >= nfull;
-        ti.nt = ti.tail ? pr : 2 * pr + r / fmd;
-        ti.m0 = (ti.tail ? fm : r % fmd) * kBM;
+        if constexpr (TAIL == 1) {
+          // pairs of column tiles: the full tiles of columns 2p and 2p + 1
+          // (m-tiles fastest), then the tail tile of pair p
+          const int per_pair = 2 * fm + tl;
+          const int pr = min(local / max(per_pair, 1), n_tiles_t - 1);
+          const int r = local - pr * per_pair;
+          const int nfull = min(2, n_tiles_n - 2 * pr) * fm;
+          const int fmd = max(fm, 1);
+          ti.tail = r >= nfull;
+          ti.nt = ti.tail ? pr : 2 * pr + r / fmd;
+          ti.m0 = (ti.tail ? fm : r % fmd) * kBM;
+        } else {
+          // column tiles in order; within one, the full m-tiles, then the
+          // tail tile of the same weight rows
+          const int per_col = fm + tl;
+          const int c = local / max(per_col, 1);
+          const int r = local - c * per_col;
+          ti.tail = tl && r == fm;
+          ti.nt = c;
+          ti.m0 = r * kBM;
+        }
         ti.tail = __builtin_amdgcn_readfirstlane(ti.tail ? 1 : 0) != 0;
         ti.g = __builtin_amdgcn_readfirstlane(ti.g);
         ti.row_base = __builtin_amdgcn_readfirstlane(ti.row_base);
@@ -384,7 +406,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   // accumulators; there a swap between the lane halves gives each lane 8
   // consecutive columns and the stores go straight out (measured faster than
   // staging for it).
-  auto epilogue = [&](const TileInfo& ti, int xr0, int col_w, unsigned char* scr) {
+  // A half tile's wave (tail tiles, Half<true>) holds 2 x 2 accumulator
+  // tiles: 32 output columns (gated: gate in tile 0, up in tile 1) or 64.
+  auto epilogue = [&](auto half, const TileInfo& ti, int xr0, int col_w, unsigned char* scr) {
+    constexpr bool kHalf = decltype(half)::value;
+    constexpr int kUp = kHalf ? 1 : 2;       // accumulator tile of the up rows of tile tn: tn + kUp
+    constexpr int kGroups = kHalf ? 1 : 2;   // 32-column tiles (gated) or 64-column pairs (down) per wave
     const GemmArgs& pr = prob(ti.p);
     const int ln = opaque_lane_id();
     const int erow = ln & 31, ehalf = ln >> 5;
@@ -402,7 +429,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         for (int i = 0; i < 4; ++i) {
           const float c0 = acc[tn][tm][4 * v4 + i];
           if constexpr (GATED)
-            o[i] = silu(c0) * acc[tn + 2][tm][4 * v4 + i];
+            o[i] = silu(c0) * acc[tn + kUp][tm][4 * v4 + i];
           else
             o[i] = c0;
         }
@@ -416,7 +443,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         const int r = xr0 + tm * 32 + erow;  // row within the tile
         const uint32_t row_off = ti.m0 + r < ti.m ? static_cast<uint32_t>(r * pr.N * 2) : kInvalid;
 #pragma unroll
-        for (int tn = 0; tn < 2; ++tn) {
+        for (int tn = 0; tn < kGroups; ++tn) {
           uint32_t pk[8];
           convert(tn, tm, pk);
 #pragma unroll
@@ -433,7 +460,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         }
       } else {
 #pragma unroll
-        for (int tp = 0; tp < 2; ++tp) {
+        for (int tp = 0; tp < kGroups; ++tp) {
 #pragma unroll
           for (int a2 = 0; a2 < 2; ++a2) {
             uint32_t pk[8];
@@ -643,12 +670,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       }
       // the W part of the tile's last stage is free until this wave loads X
       // of the stage three ahead into its own 4 KB of it
-      epilogue(cur, xrow0, cur.nt * OUT_COLS + wn * WCOLS, part_ptr(2 * (j - 1) + 1) + wave * 4096);
+      epilogue(Half<false>{}, cur, xrow0, cur.nt * OUT_COLS + wn * WCOLS, part_ptr(2 * (j - 1) + 1) + wave * 4096);
       zero_acc();
     }
   };
 
-  // ---- tail tiles: 128 token rows x 512 weight rows ----
+  // ---- wide tail tiles (TAIL 1): 128 token rows x 512 weight rows ----
   // Two stages of 80 KB: X [128 rows x 128 B] at 0, W [512 rows x 128 B] at
   // 16 KB, the same chunk swizzle as the full parts.  Wave w fills X rows
   // 16w .. 16w+15 (two loads) and W rows 64w .. 64w+63 (eight loads, all
@@ -658,128 +685,282 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   // first MFMAs of stage j into the other stage buffer, read last in stage
   // j - 1.  (Stages of 32 along K, four in flight in 40 KB buffers, were
   // measured no faster.)
-  constexpr int T_XROWS = kBM / 2, T_WROWS = 2 * kBN;
-  constexpr int T_XPART = T_XROWS * C::ROW;             // 16 KB
-  constexpr int T_STAGE = T_XPART + T_WROWS * C::ROW;   // 80 KB
-  constexpr int T_XL = T_XROWS / C::RPI / 8;            // X loads per wave and stage: 2
-  constexpr int T_WL = T_WROWS / C::RPI / 8;            // W loads per wave and stage: 8
-  constexpr int OUT_COLS_T = 2 * OUT_COLS;
-  static_assert(2 * T_STAGE <= C::LDS, "two tail stages fit the LDS");
-  const int wm_t = wave & 1, wn_t = wave >> 1;
-  const int xrow0_t = wm_t * 64, wrow0_t = wn_t * 128;
-  auto t_buf = [&](int b) { return smem + b * T_STAGE; };
-  auto t_read_frags = [&](int b, int ks, int set) {
-    const unsigned char* xp = t_buf(b);
-    const unsigned char* wp = xp + T_XPART;
-    const int slot = ((2 * ks + lhalf) ^ rsw) << 4;
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-      wf[set][t] = as_bf16x8(*reinterpret_cast<const u32x4*>(wp + (wrow0_t + t * 32 + lrow) * C::ROW + slot));
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-      xf[set][t] = as_bf16x8(*reinterpret_cast<const u32x4*>(xp + (xrow0_t + t * 32 + lrow) * C::ROW + slot));
-  };
-  auto tail_run = [&]() {
-    __amdgpu_buffer_rsrc_t trs_x, trs_w;
-    uint32_t txoff[T_XL], twoff[T_WL];
-    int tt = first, tkb = 0;
-    uint32_t tk0 = 0, tk1 = 0;
-    // gathered source rows one tile ahead, as for the full tiles
-    int txr_next[T_XL];
-    auto t_rows_of = [&](int t) {
-      const TileInfo ti = tile_info(t);
-      const int ln = opaque_lane_id();
-#pragma unroll
-      for (int i = 0; i < T_XL; ++i) {
-        const int r = 16 * wave + C::RPI * i + ln / C::CPR;
-        txr_next[i] = a.x_rows[ti.row_base + (ti.m0 + r < ti.m ? ti.m0 + r : 0)];
-      }
+  auto tail_run_wide = [&]() {
+    constexpr int T_XROWS = kBM / 2, T_WROWS = 2 * kBN;
+    constexpr int T_XPART = T_XROWS * C::ROW;             // 16 KB
+    constexpr int T_STAGE = T_XPART + T_WROWS * C::ROW;   // 80 KB
+    constexpr int T_XL = T_XROWS / C::RPI / 8;            // X loads per wave and stage: 2
+    constexpr int T_WL = T_WROWS / C::RPI / 8;            // W loads per wave and stage: 8
+    constexpr int OUT_COLS_T = 2 * OUT_COLS;
+    static_assert(2 * T_STAGE <= C::LDS, "two tail stages fit the LDS");
+    const int wm_t = wave & 1, wn_t = wave >> 1;
+    const int xrow0_t = wm_t * 64, wrow0_t = wn_t * 128;
+    auto t_buf = [&](int b) { return smem + b * T_STAGE; };
+    auto t_read_frags = [&](int b, int ks, int set) {
+      const unsigned char* xp = t_buf(b);
+      const unsigned char* wp = xp + T_XPART;
+      const int slot = ((2 * ks + lhalf) ^ rsw) << 4;
+  #pragma unroll
+      for (int t = 0; t < 4; ++t)
+        wf[set][t] = as_bf16x8(*reinterpret_cast<const u32x4*>(wp + (wrow0_t + t * 32 + lrow) * C::ROW + slot));
+  #pragma unroll
+      for (int t = 0; t < 2; ++t)
+        xf[set][t] = as_bf16x8(*reinterpret_cast<const u32x4*>(xp + (xrow0_t + t * 32 + lrow) * C::ROW + slot));
     };
-    auto t_setup = [&](int t_in, bool prefetched) {
-      const bool live = t_in < run_end;
-      const uint32_t dead = live ? 0u : kInvalid;
-      const TileInfo ti = tile_info(live ? t_in : run_start);
-      const int ln = opaque_lane_id();
-      const uint16_t* xb = a.x_rows ? a.x : a.x + static_cast<size_t>(ti.row_base + ti.m0) * a.K;
-      trs_x = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(xb), 0, kRecords, kRsrcWord3);
-      if (a.x_rows && live && !prefetched) t_rows_of(t_in);
-#pragma unroll
-      for (int i = 0; i < T_XL; ++i) {
-        const int r = 16 * wave + C::RPI * i + ln / C::CPR;
-        const int xr = a.x_rows ? txr_next[i] : r;
-        txoff[i] = (live && ti.m0 + r < ti.m) ? static_cast<uint32_t>(xr * a.K * 2 + chunk_of(i, ln) * 16) : kInvalid;
-      }
-      if (a.x_rows && t_in + static_cast<int>(gridDim.x) < run_end) t_rows_of(t_in + gridDim.x);
-      const int col0 = ti.nt * OUT_COLS_T;
-      const size_t gofs = static_cast<size_t>(ti.g) * a.group_stride + static_cast<size_t>(col0) * a.ldw;
-      const bool up = GATED && (wave & 1);  // W rows 64w .. 64w+63: gate rows for even w, up rows for odd w
-      trs_w = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>((up ? a.w1 : a.w0) + gofs), 0, kRecords,
-                                                kRsrcWord3);
-#pragma unroll
-      for (int i = 0; i < T_WL; ++i) {
-        const int r = 64 * wave + C::RPI * i + ln / C::CPR;
-        const int lcol = GATED ? (r >> 7) * 64 + (r & 63) : r;
-        twoff[i] =
-            ((col0 + lcol < a.N) ? static_cast<uint32_t>(lcol * a.ldw * 2 + chunk_of(i, ln) * 16) : kInvalid) | dead;
-      }
-    };
-    auto t_kstep = [&]() {
-      const uint32_t k = static_cast<uint32_t>(tkb * C::BK * 2);
-      tk0 = k | kmask(tkb, 0, a.K);
-      tk1 = k | kmask(tkb, 1, a.K);
-    };
-    auto t_advance = [&]() {
-      if (++tkb == nkb_g) {
-        tkb = 0;
-        tt += gridDim.x;
-        t_setup(tt, true);
-      }
-      t_kstep();
-    };
-    auto t_load = [&](int b, int i) {  // load i < T_XL: X, else W load i - T_XL
-      const uint32_t k = (i & 1) ? tk1 : tk0;
-      if (i < T_XL)
-        load_lds16(trs_x, t_buf(b) + wave * (16 * C::ROW) + i * 1024, (txoff[i] + k) | (k & kInvalid));
-      else
-        load_lds16(trs_w, t_buf(b) + T_XPART + wave * (64 * C::ROW) + (i - T_XL) * 1024,
-                   (twoff[i - T_XL] + k) | (k & kInvalid));
-    };
-    zero_acc();
-    tt = run_start;
-    tkb = 0;
-    t_setup(tt, false);
-    t_kstep();
-#pragma unroll
-    for (int i = 0; i < T_XL + T_WL; ++i) t_load(0, i);
-    t_advance();
-    __builtin_amdgcn_s_waitcnt(kWaitAll);
-    phase_barrier();
-    int j = 0;
-    for (int t = run_start; t < run_end; t += gridDim.x) {
-      const TileInfo cur = tile_info(t);
-      for (int kb = 0; kb < nkb_g; ++kb, ++j) {
-        const int b = j & 1;
-        t_read_frags(b, 0, 0);
-#pragma unroll
-        for (int ks = 0; ks < C::KSTEPS; ++ks) {
-          if (ks + 1 < C::KSTEPS) t_read_frags(b, ks + 1, (ks + 1) & 1);
-          // stage j + 1's ten loads in the first three K-steps (4, 4, 2),
-          // so that they have landed by the end of the stage
-          constexpr int kFirst[5] = {0, 4, 8, 10, 10};
-#pragma unroll
-          for (int i = kFirst[ks]; i < kFirst[ks + 1]; ++i) t_load(b ^ 1, i);
-          mfma_set(ks & 1);
-          __builtin_amdgcn_sched_barrier(0);
+    auto run = [&]() {
+      __amdgpu_buffer_rsrc_t trs_x, trs_w;
+      uint32_t txoff[T_XL], twoff[T_WL];
+      int tt = first, tkb = 0;
+      uint32_t tk0 = 0, tk1 = 0;
+      // gathered source rows one tile ahead, as for the full tiles
+      int txr_next[T_XL];
+      auto t_rows_of = [&](int t) {
+        const TileInfo ti = tile_info(t);
+        const int ln = opaque_lane_id();
+  #pragma unroll
+        for (int i = 0; i < T_XL; ++i) {
+          const int r = 16 * wave + C::RPI * i + ln / C::CPR;
+          txr_next[i] = a.x_rows[ti.row_base + (ti.m0 + r < ti.m ? ti.m0 + r : 0)];
         }
-        t_advance();
-        __builtin_amdgcn_s_waitcnt(kWaitAll);  // own stage j+1 landed, LDS reads done
-        phase_barrier();
-      }
-      // the buffer of the tile's last stage is free until the next loads
-      // into it; this wave's own W rows there are its 8 KB
-      epilogue(cur, xrow0_t, cur.nt * OUT_COLS_T + wn_t * WCOLS, t_buf((j - 1) & 1) + T_XPART + wave * (64 * C::ROW));
+      };
+      auto t_setup = [&](int t_in, bool prefetched) {
+        const bool live = t_in < run_end;
+        const uint32_t dead = live ? 0u : kInvalid;
+        const TileInfo ti = tile_info(live ? t_in : run_start);
+        const int ln = opaque_lane_id();
+        const uint16_t* xb = a.x_rows ? a.x : a.x + static_cast<size_t>(ti.row_base + ti.m0) * a.K;
+        trs_x = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(xb), 0, kRecords, kRsrcWord3);
+        if (a.x_rows && live && !prefetched) t_rows_of(t_in);
+  #pragma unroll
+        for (int i = 0; i < T_XL; ++i) {
+          const int r = 16 * wave + C::RPI * i + ln / C::CPR;
+          const int xr = a.x_rows ? txr_next[i] : r;
+          txoff[i] = (live && ti.m0 + r < ti.m) ? static_cast<uint32_t>(xr * a.K * 2 + chunk_of(i, ln) * 16) : kInvalid;
+        }
+        if (a.x_rows && t_in + static_cast<int>(gridDim.x) < run_end) t_rows_of(t_in + gridDim.x);
+        const int col0 = ti.nt * OUT_COLS_T;
+        const size_t gofs = static_cast<size_t>(ti.g) * a.group_stride + static_cast<size_t>(col0) * a.ldw;
+        const bool up = GATED && (wave & 1);  // W rows 64w .. 64w+63: gate rows for even w, up rows for odd w
+        trs_w = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>((up ? a.w1 : a.w0) + gofs), 0, kRecords,
+                                                  kRsrcWord3);
+  #pragma unroll
+        for (int i = 0; i < T_WL; ++i) {
+          const int r = 64 * wave + C::RPI * i + ln / C::CPR;
+          const int lcol = GATED ? (r >> 7) * 64 + (r & 63) : r;
+          twoff[i] =
+              ((col0 + lcol < a.N) ? static_cast<uint32_t>(lcol * a.ldw * 2 + chunk_of(i, ln) * 16) : kInvalid) | dead;
+        }
+      };
+      auto t_kstep = [&]() {
+        const uint32_t k = static_cast<uint32_t>(tkb * C::BK * 2);
+        tk0 = k | kmask(tkb, 0, a.K);
+        tk1 = k | kmask(tkb, 1, a.K);
+      };
+      auto t_advance = [&]() {
+        if (++tkb == nkb_g) {
+          tkb = 0;
+          tt += gridDim.x;
+          t_setup(tt, true);
+        }
+        t_kstep();
+      };
+      auto t_load = [&](int b, int i) {  // load i < T_XL: X, else W load i - T_XL
+        const uint32_t k = (i & 1) ? tk1 : tk0;
+        if (i < T_XL)
+          load_lds16(trs_x, t_buf(b) + wave * (16 * C::ROW) + i * 1024, (txoff[i] + k) | (k & kInvalid));
+        else
+          load_lds16(trs_w, t_buf(b) + T_XPART + wave * (64 * C::ROW) + (i - T_XL) * 1024,
+                     (twoff[i - T_XL] + k) | (k & kInvalid));
+      };
       zero_acc();
-    }
+      tt = run_start;
+      tkb = 0;
+      t_setup(tt, false);
+      t_kstep();
+  #pragma unroll
+      for (int i = 0; i < T_XL + T_WL; ++i) t_load(0, i);
+      t_advance();
+      __builtin_amdgcn_s_waitcnt(kWaitAll);
+      phase_barrier();
+      int j = 0;
+      for (int t = run_start; t < run_end; t += gridDim.x) {
+        const TileInfo cur = tile_info(t);
+        for (int kb = 0; kb < nkb_g; ++kb, ++j) {
+          const int b = j & 1;
+          t_read_frags(b, 0, 0);
+  #pragma unroll
+          for (int ks = 0; ks < C::KSTEPS; ++ks) {
+            if (ks + 1 < C::KSTEPS) t_read_frags(b, ks + 1, (ks + 1) & 1);
+            // stage j + 1's ten loads in the first three K-steps (4, 4, 2),
+            // so that they have landed by the end of the stage
+            constexpr int kFirst[5] = {0, 4, 8, 10, 10};
+  #pragma unroll
+            for (int i = kFirst[ks]; i < kFirst[ks + 1]; ++i) t_load(b ^ 1, i);
+            mfma_set(ks & 1);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+          t_advance();
+          __builtin_amdgcn_s_waitcnt(kWaitAll);  // own stage j+1 landed, LDS reads done
+          phase_barrier();
+        }
+        // the buffer of the tile's last stage is free until the next loads
+        // into it; this wave's own W rows there are its 8 KB
+        epilogue(Half<false>{}, cur, xrow0_t, cur.nt * OUT_COLS_T + wn_t * WCOLS,
+                 t_buf((j - 1) & 1) + T_XPART + wave * (64 * C::ROW));
+        zero_acc();
+      }
+    };
+    run();
+  };
+
+  // ---- half tail tiles (TAIL 2): 128 token rows x 256 weight rows ----
+  // Stages of 48 KB, three in a ring: X [128 rows x 128 B] at 0, W [256
+  // rows x 128 B] at 16 KB, the same chunk swizzle as the full parts.  Wave w
+  // fills X rows 16w .. 16w+15 (two loads) and W rows 32w .. 32w+31 (four
+  // loads, all gate or all up rows).  Gated, W row r holds the gate (r / 32
+  // even) or up row of column 32 (r / 64) + r % 32, so that each 64-row
+  // quarter holds the gate and up rows of 32 columns.  Wave (wm_t, wn_t) =
+  // (w & 1, w >> 1) owns token rows 64 wm_t .. +63 and W rows 64 wn_t .. +63:
+  // 2 x 2 MFMA tiles, half a full tile's work.  The loads of stage j + 2 go
+  // out among the MFMAs of stage j into the buffer read last in stage j - 1;
+  // before the barrier that ends stage j each wave waits for its loads of
+  // stage j + 1.  A tail tile follows the full m-tiles of its column tile,
+  // so it reads the same weight rows at about the same time.
+  auto tail_run_half = [&]() {
+    constexpr int T_XROWS = kBM / 2, T_WROWS = kBN;
+    constexpr int T_XPART = T_XROWS * C::ROW;             // 16 KB
+    constexpr int T_STAGE = T_XPART + T_WROWS * C::ROW;   // 48 KB
+    constexpr int T_NBUF = 3;
+    constexpr int T_XL = T_XROWS / C::RPI / 8;            // X loads per wave and stage: 2
+    constexpr int T_WL = T_WROWS / C::RPI / 8;            // W loads per wave and stage: 4
+    constexpr int T_LOADS = T_XL + T_WL;
+    static_assert(T_NBUF * T_STAGE <= C::LDS, "three tail stages fit the LDS");
+    const int wm_t = wave & 1, wn_t = wave >> 1;
+    const int xrow0_t = wm_t * 64, wrow0_t = wn_t * 64;
+    auto t_buf = [&](int s) { return smem + (s % T_NBUF) * T_STAGE; };
+    auto t_read_frags = [&](int s, int ks, int set) {
+      const unsigned char* xp = t_buf(s);
+      const unsigned char* wp = xp + T_XPART;
+      const int slot = ((2 * ks + lhalf) ^ rsw) << 4;
+  #pragma unroll
+      for (int t = 0; t < 2; ++t)
+        wf[set][t] = as_bf16x8(*reinterpret_cast<const u32x4*>(wp + (wrow0_t + t * 32 + lrow) * C::ROW + slot));
+  #pragma unroll
+      for (int t = 0; t < 2; ++t)
+        xf[set][t] = as_bf16x8(*reinterpret_cast<const u32x4*>(xp + (xrow0_t + t * 32 + lrow) * C::ROW + slot));
+    };
+    auto t_mfma_set = [&](int set) {
+  #pragma unroll
+      for (int tn = 0; tn < 2; ++tn)
+  #pragma unroll
+        for (int tm = 0; tm < 2; ++tm) acc[tn][tm] = mfma32x32x16(wf[set][tn], xf[set][tm], acc[tn][tm]);
+    };
+    auto run = [&]() {
+      __amdgpu_buffer_rsrc_t trs_x, trs_w;
+      uint32_t txoff[T_XL], twoff[T_WL];
+      int tt = first, tkb = 0;
+      uint32_t tk0 = 0, tk1 = 0;
+      // gathered source rows one tile ahead, as for the full tiles
+      int txr_next[T_XL];
+      auto t_rows_of = [&](int t) {
+        const TileInfo ti = tile_info(t);
+        const int ln = opaque_lane_id();
+  #pragma unroll
+        for (int i = 0; i < T_XL; ++i) {
+          const int r = 16 * wave + C::RPI * i + ln / C::CPR;
+          txr_next[i] = a.x_rows[ti.row_base + (ti.m0 + r < ti.m ? ti.m0 + r : 0)];
+        }
+      };
+      auto t_setup = [&](int t_in, bool prefetched) {
+        const bool live = t_in < run_end;
+        const uint32_t dead = live ? 0u : kInvalid;
+        const TileInfo ti = tile_info(live ? t_in : run_start);
+        const int ln = opaque_lane_id();
+        const uint16_t* xb = a.x_rows ? a.x : a.x + static_cast<size_t>(ti.row_base + ti.m0) * a.K;
+        trs_x = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(xb), 0, kRecords, kRsrcWord3);
+        if (a.x_rows && live && !prefetched) t_rows_of(t_in);
+  #pragma unroll
+        for (int i = 0; i < T_XL; ++i) {
+          const int r = 16 * wave + C::RPI * i + ln / C::CPR;
+          const int xr = a.x_rows ? txr_next[i] : r;
+          txoff[i] = (live && ti.m0 + r < ti.m) ? static_cast<uint32_t>(xr * a.K * 2 + chunk_of(i, ln) * 16) : kInvalid;
+        }
+        if (a.x_rows && t_in + static_cast<int>(gridDim.x) < run_end) t_rows_of(t_in + gridDim.x);
+        const int col0 = ti.nt * OUT_COLS;
+        const size_t gofs = static_cast<size_t>(ti.g) * a.group_stride + static_cast<size_t>(col0) * a.ldw;
+        const bool up = GATED && (wave & 1);  // W rows 32w .. 32w+31: gate rows for even w, up rows for odd w
+        trs_w = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>((up ? a.w1 : a.w0) + gofs), 0, kRecords,
+                                                  kRsrcWord3);
+  #pragma unroll
+        for (int i = 0; i < T_WL; ++i) {
+          const int r = 32 * wave + C::RPI * i + ln / C::CPR;
+          const int lcol = GATED ? (r >> 6) * 32 + (r & 31) : r;
+          twoff[i] =
+              ((col0 + lcol < a.N) ? static_cast<uint32_t>(lcol * a.ldw * 2 + chunk_of(i, ln) * 16) : kInvalid) | dead;
+        }
+      };
+      auto t_kstep = [&]() {
+        const uint32_t k = static_cast<uint32_t>(tkb * C::BK * 2);
+        tk0 = k | kmask(tkb, 0, a.K);
+        tk1 = k | kmask(tkb, 1, a.K);
+      };
+      auto t_advance = [&]() {
+        if (++tkb == nkb_g) {
+          tkb = 0;
+          tt += gridDim.x;
+          t_setup(tt, true);
+        }
+        t_kstep();
+      };
+      auto t_load = [&](int s, int i) {  // load i < T_XL: X, else W load i - T_XL
+        const uint32_t k = (i & 1) ? tk1 : tk0;
+        if (i < T_XL)
+          load_lds16(trs_x, t_buf(s) + wave * (16 * C::ROW) + i * 1024, (txoff[i] + k) | (k & kInvalid));
+        else
+          load_lds16(trs_w, t_buf(s) + T_XPART + wave * (32 * C::ROW) + (i - T_XL) * 1024,
+                     (twoff[i - T_XL] + k) | (k & kInvalid));
+      };
+      zero_acc();
+      tt = run_start;
+      tkb = 0;
+      t_setup(tt, false);
+      t_kstep();
+      // stages 0 and 1
+      for (int s = 0; s < 2; ++s) {
+  #pragma unroll
+        for (int i = 0; i < T_LOADS; ++i) t_load(s, i);
+        t_advance();
+      }
+      __builtin_amdgcn_s_waitcnt(wait_vm(T_LOADS));  // own stage-0 loads landed
+      phase_barrier();
+      int j = 0;
+      for (int t = run_start; t < run_end; t += gridDim.x) {
+        const TileInfo cur = tile_info(t);
+        for (int kb = 0; kb < nkb_g; ++kb, ++j) {
+          t_read_frags(j, 0, 0);
+  #pragma unroll
+          for (int ks = 0; ks < C::KSTEPS; ++ks) {
+            if (ks + 1 < C::KSTEPS) t_read_frags(j, ks + 1, (ks + 1) & 1);
+            // stage j + 2's six loads in the first three K-steps, two each
+            constexpr int kFirst[5] = {0, 2, 4, 6, 6};
+  #pragma unroll
+            for (int i = kFirst[ks]; i < kFirst[ks + 1]; ++i) t_load(j + 2, i);
+            t_mfma_set(ks & 1);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+          t_advance();
+          __builtin_amdgcn_s_waitcnt(wait_vm(T_LOADS));  // own stage j+1 landed
+          __builtin_amdgcn_s_waitcnt(kWaitLgkm0);        // this stage's LDS reads done
+          phase_barrier();
+        }
+        // the buffer of the tile's last stage is free until the loads of the
+        // stage three ahead; this wave's own W rows there are its 4 KB
+        epilogue(Half<true>{}, cur, xrow0_t, cur.nt * OUT_COLS + wn_t * (WCOLS / 2),
+                 t_buf(j - 1) + T_XPART + wave * (32 * C::ROW));
+        zero_acc();
+      }
+    };
+    run();
   };
 
   // ---- runs ----
@@ -796,10 +977,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     }
     run_start = t;
     run_end = e;
-    if (TAIL && tail)
-      tail_run();
-    else
+    if constexpr (TAIL == 1) {
+      if (tail) tail_run_wide();
+      else full_run();
+    } else if constexpr (TAIL == 2) {
+      if (tail) tail_run_half();
+      else full_run();
+    } else {
       full_run();
+    }
     __builtin_amdgcn_s_waitcnt(kWaitAll);
     phase_barrier();
     t = e;
@@ -823,7 +1009,7 @@ int device_cu_count() {
   return n;
 }
 
-template <bool GATED, int PFX, bool PAIR, bool SBLK, bool TAIL>
+template <bool GATED, int PFX, bool PAIR, bool SBLK, int TAIL>
 hipError_t launch_pfx_t(const TiledArgs& ta, long long grid, hipStream_t st) {
   static unsigned long long lds_set = 0;  // devices with the LDS limit raised
   const hipError_t e_lds =
@@ -841,15 +1027,23 @@ template <bool GATED, int PFX>
 hipError_t launch_pfx(const TiledArgs& ta, long long grid, hipStream_t st) {
   if (ta.g.offsets == nullptr) {
     if constexpr (PFX == 1) {
-      if (ta.sp_tiles == 0) return launch_pfx_t<GATED, 1, false, true, false>(ta, grid, st);
+      if (ta.sp_tiles == 0) return launch_pfx_t<GATED, 1, false, true, 0>(ta, grid, st);
     }
-    return launch_pfx_t<GATED, PFX, true, false, false>(ta, grid, st);
+    return launch_pfx_t<GATED, PFX, true, false, 0>(ta, grid, st);
   }
   // (with the shared experts' tiles in the same launch the two-problem
   // kernel keeps whole tiles: its tail variant needs more registers than
-  // two waves per SIMD allow)
-  if (ta.sp_tiles > 0) return launch_pfx_t<GATED, PFX, true, false, false>(ta, grid, st);
-  return launch_pfx_t<GATED, PFX, false, false, true>(ta, grid, st);
+  // two waves per SIMD allow; so does the tail variant with 16 prefix
+  // entries per lane, for more than 256 groups)
+  if constexpr (PFX > 4) {
+    return launch_pfx_t<GATED, PFX, true, false, 0>(ta, grid, st);
+  } else {
+    if (ta.sp_tiles > 0) return launch_pfx_t<GATED, PFX, true, false, 0>(ta, grid, st);
+    // long K: half tail tiles, which keep pace with the full tiles of their
+    // weight rows; otherwise wide tail tiles, fewer of them (both measured)
+    if (ta.g.K >= kHalfTailK) return launch_pfx_t<GATED, PFX, false, false, 2>(ta, grid, st);
+    return launch_pfx_t<GATED, PFX, false, false, 1>(ta, grid, st);
+  }
 }
 
 // Host-side checks of one problem: no blocked layouts, at most kMaxGroups
