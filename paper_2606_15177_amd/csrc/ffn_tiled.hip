@@ -173,11 +173,10 @@ struct TiledArgs {
 //    and 2p + 1 (m-tiles fastest), then the tail tile that covers both.
 //    Two 80 KB stages: X [128 x 64], W [512 x 64].
 //  - TAIL 2, half: 128 x 256 weight rows.  Within a group the tiles go by
-//    column tiles, m-tiles fastest, the tail tile last.  With half a full
-//    tile's work per stage it keeps pace with the full tiles that read the
-//    same weight rows and finds them in L2; a wide tail tile falls behind
-//    them on long K and reads its weights from HBM.  Three 48 KB stages:
-//    X [128 x 64], W [256 x 64].
+//    column tiles, m-tiles fastest, the tail tile last.  Three 48 KB stages:
+//    X [128 x 64], W [256 x 64].  On long K a wide tail tile, with 80 KB
+//    per stage, waits on weight rows that miss L2 and takes 1.28 times a
+//    full tile; a half tile takes 0.58 times a full tile for half its work.
 template <bool GATED, int kPfx, bool PAIR, bool SBLK, int TAIL>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void tiled_kernel(TiledArgs ta) {
   using C = Stage;
