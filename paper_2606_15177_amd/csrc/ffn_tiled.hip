@@ -238,7 +238,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       mt_end[i] = g < a.groups ? carry + inc : 0x7fffffff;
       carry += __shfl(inc, kWave - 1);
     }
-    total_mt = carry;
+    total_mt = __builtin_amdgcn_readfirstlane(carry);  // equal in every lane; the compiler cannot tell
   }
   // tiles of g: with TAIL the prefix already counts tiles
   const int total_tiles = sp_tiles + ((TAIL && a.offsets != nullptr) ? total_mt : total_mt * n_tiles_n);
@@ -253,6 +253,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   };
   // group of tile t: the number of groups whose tiles all precede t
   auto tile_info = [&](int t_all) {
+    // tile ids are wave-uniform: stated here, every branch on them is uniform
+    // and so are the buffer descriptors built from the tile (else the
+    // compiler may wrap each load in a loop over the lanes' descriptors)
+    t_all = __builtin_amdgcn_readfirstlane(t_all);
     TileInfo ti;
     ti.tail = false;
     ti.p = (PAIR && t_all < sp_tiles) ? 0 : 1;

@@ -79,6 +79,11 @@ def _run_ffn(moe, cfg, wl, idx):
     (500, 256, 3, 2, 4096, 3, 0, 0),
     (500, 4096, 3, 2, 200, 3, 0, 0),         # ... with ragged N
     (500, 200, 3, 2, 4096, 3, 0, 0),
+    # the shared experts' tiles in the routed launch, groups with short
+    # remainders (whole tiles there), short and long K
+    (500, 256, 3, 2, 256, 3, 1, 256),
+    (500, 4096, 3, 2, 256, 3, 1, 200),
+    (500, 200, 3, 2, 4096, 3, 1, 4096),
     # the tiled kernel's group lookup holds 1, 4 or 16 prefix entries per lane
     (2048, 128, 128, 8, 128, 128, 0, 0),     # 65..256 groups
     (4096, 128, 300, 8, 128, 300, 0, 0),     # 257..1024 groups
