@@ -110,10 +110,16 @@ def stage_work(cfg, R: int, active: int) -> dict:
     n_sh, I_sh = cfg.n_shared, (cfg.I_shared if cfg.n_shared else 0)
     bf = 2
     w = {}
-    w["route"] = dict(bytes=T * E * 4 + T * 4 + T * k * 8 + 2 * S * E * 8, flops=0)
+    # the statistics (src read, counts read and written) go with the stage
+    # that counts them: the router for batches it dispatches itself (at most
+    # 512 pairs), else the dispatch's count pass
+    stats_bytes = T * 4 + 2 * S * E * 8
+    stats_in_route = T * k <= 512
+    w["route"] = dict(bytes=T * E * 4 + T * k * 8 + (stats_bytes if stats_in_route else 0), flops=0)
     # the dispatch sort only: the token rows are read by the gate/up GEMM
     # through perm_token (counted there as R*H*bf), never copied
-    w["permute"] = dict(bytes=T * k * 4 + (cfg.E_local + 1) * 4 + R * 4 + T * k * 4, flops=0)
+    w["permute"] = dict(bytes=T * k * 4 + (cfg.E_local + 1) * 4 + R * 4 + T * k * 4
+                        + (0 if stats_in_route else stats_bytes), flops=0)
     w["ffn_up"] = dict(bytes=active * 2 * I * H * bf + n_sh * 2 * I_sh * H * bf + R * H * bf
                        + (T * H * bf if n_sh else 0) + R * I * bf + T * n_sh * I_sh * bf,
                        flops=2 * 2 * H * I * R + 2 * 2 * H * n_sh * I_sh * T)
@@ -446,10 +452,17 @@ def bench_layer(args, watch) -> int:
     # timed steps carry only the dominant kernel's pair).
     n_probe = max(3, min(args.steps, 10))
     ev_flags = 0 if args.fenced_events else HIP_EVENT_DISABLE_SYSTEM_FENCE
-    probe_ev = HipEvents(n_ev * n_probe, ev_flags)
+    # Probe i runs the layer twice: with the source x expert statistics
+    # (events i), then without them (events n_probe + i); alternating keeps
+    # the two sets under the same clocks.  Route + permute of the first
+    # against the second is the cost of collecting A (counted in the route
+    # kernel, or in the dispatch's count pass when the dispatch takes several
+    # blocks).
+    probe_ev = HipEvents(2 * n_ev * n_probe, ev_flags)
     for i in range(n_probe):
-        layer.forward(logits, src, x, counts, out,
-                      moe.make_taps(offsets=offsets, events=probe_ev.ev[i * n_ev:(i + 1) * n_ev]))
+        for j, cts in ((i, counts), (n_probe + i, None)):
+            layer.forward(logits, src, x, cts, out,
+                          moe.make_taps(offsets=offsets, events=probe_ev.ev[j * n_ev:(j + 1) * n_ev]))
     torch.cuda.synchronize()
     stage_ms = {}
     for s_i, name in enumerate(STAGES):
@@ -457,14 +470,11 @@ def bench_layer(args, watch) -> int:
         stage_ms[name] = sum(vals) / len(vals)
     # GPU time of each probe step: first stage's start to the last stage's end
     probe_steps = sorted(probe_ev.elapsed_ms(i * n_ev, i * n_ev + n_ev - 1) for i in range(n_probe))
-    # the same probe without the source x expert statistics (the counting that
-    # the route kernel fuses): its route time against the one above is the
-    # cost of collecting A
-    for i in range(n_probe):
-        layer.forward(logits, src, x, None, out,
-                      moe.make_taps(offsets=offsets, events=probe_ev.ev[i * n_ev:(i + 1) * n_ev]))
-    torch.cuda.synchronize()
-    route_no_stats = sum(probe_ev.elapsed_ms(i * n_ev, i * n_ev + 1) for i in range(n_probe)) / n_probe
+
+    def route_permute_ms(first):
+        return sum(probe_ev.elapsed_ms(j * n_ev, j * n_ev + 3) for j in range(first, first + n_probe)) / n_probe
+    rp_stats = route_permute_ms(0)
+    rp_no_stats = route_permute_ms(n_probe)
     probe_ev.close()
     dom = max(STAGES, key=lambda n: stage_ms[n])
     dom_i = STAGES.index(dom)
@@ -614,8 +624,10 @@ def bench_layer(args, watch) -> int:
                  "note": "back-to-back steps, wall clock"},
         "step_gpu_ms_warm_probe": {"median": round(probe_steps[len(probe_steps) // 2], 4),
                                    "min": round(probe_steps[0], 4), "samples": len(probe_steps)},
-        "stats_collection": {"route_ms_with_counts": round(stage_ms["route"], 4),
-                             "route_ms_without_counts": round(route_no_stats, 4)},
+        "stats_collection": {"route_permute_ms_with_counts": round(rp_stats, 4),
+                             "route_permute_ms_without_counts": round(rp_no_stats, 4),
+                             "overhead_ms": round(rp_stats - rp_no_stats, 4),
+                             "counted_in": "route" if cfg.T * cfg.k <= 512 else "dispatch count pass"},
         **({"gpu_metrics": watch.stop()} if watch else {}),
         "rows_local": R,
         "active_experts": active,

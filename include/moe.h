@@ -143,8 +143,9 @@ enum moe_entry { MOE_ENTRY_PERMUTE = 1, MOE_ENTRY_EXPERT_FFN = 2, MOE_ENTRY_FORW
 
 /* Stages of moe_forward, for the optional timing events of moe_taps. */
 enum moe_stage {
-    MOE_STAGE_ROUTE = 0,    /* top-k gating + source x expert counts */
-    MOE_STAGE_PERMUTE = 1,  /* slot counts, offsets, stable dispatch order, row gather */
+    MOE_STAGE_ROUTE = 0,    /* top-k gating (+ the source x expert counts when T*k <= 512) */
+    MOE_STAGE_PERMUTE = 1,  /* slot counts (+ the source x expert counts when T*k > 512),
+                               offsets, stable dispatch order */
     MOE_STAGE_FFN_UP = 2,   /* gate/up GEMM with the SwiGLU epilogue (routed, then shared) */
     MOE_STAGE_FFN_DOWN = 3, /* down GEMM (routed, then shared) */
     MOE_STAGE_COMBINE = 4,  /* weighted combine back to token order */

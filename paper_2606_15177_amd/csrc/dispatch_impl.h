@@ -7,6 +7,35 @@
 
 namespace moe {
 
+// Source x expert statistics (Sec. 5.1, the matrices A_{l,s,e} and B_{l,e}):
+// a block counts its pairs into an S x E int32 histogram in LDS when it has
+// at most kLdsBinsMax bins (else straight into the global counts) and then
+// flushes the non-zero bins with one 64-bit atomic add each.  Integer
+// atomics make the result independent of the order in which blocks land.
+constexpr int kLdsBinsMax = 16384;  // S*E bins kept in LDS (64 KB)
+
+__device__ __forceinline__ void count_pair(int s, int e, int S, int E, bool use_lds, int* hist,
+                                           unsigned long long* counts, int32_t* expert_load) {
+  if (s < 0 || s >= S || e < 0 || e >= E) return;
+  if (use_lds) {
+    atomicAdd(&hist[s * E + e], 1);
+  } else {
+    atomicAdd(&counts[static_cast<size_t>(s) * E + e], 1ull);
+    if (expert_load) atomicAdd(&expert_load[e], 1);
+  }
+}
+
+__device__ __forceinline__ void flush_hist(const int* hist, int bins, int E,
+                                           unsigned long long* counts, int32_t* expert_load) {
+  for (int b = threadIdx.x; b < bins; b += blockDim.x) {
+    const int c = hist[b];
+    if (c) {
+      atomicAdd(&counts[b], static_cast<unsigned long long>(c));
+      if (expert_load) atomicAdd(&expert_load[b % E], c);
+    }
+  }
+}
+
 // slot_of[e] = local slot hosting expert e, or -1.  An expert listed twice
 // (outside the documented contract) resolves to its lowest slot, the same in
 // every kernel, so the count and scatter passes always agree.  Ends with a

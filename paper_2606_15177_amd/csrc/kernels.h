@@ -29,6 +29,8 @@ struct DispatchArgs {
 };
 // Batches of at most this many (token, expert) pairs are dispatched by one block.
 constexpr int kDispatchPairs = 512;
+// Experts per layer (E, and so E_local) that the kernels take.
+constexpr int kMaxExperts = 1024;
 
 // Top-k selection + gates; when counts != nullptr also accumulates the
 // source x expert counts (and sets expert_load if non-null, which must have
@@ -49,10 +51,14 @@ hipError_t launch_fill_i32(int32_t* p, int n, int32_t value, hipStream_t st);
 
 // ---- permute.hip -----------------------------------------------------------
 size_t permute_ws_bytes(int T, int k, int E_local);
-// offsets / perm_token / inv_pos of the stable dispatch sort.
+// offsets / perm_token / inv_pos of the stable dispatch sort.  With counts
+// != nullptr the count pass also accumulates the source x expert counts of
+// all T*k pairs (and adds to expert_load as launch_route does); only for
+// T*k > kDispatchPairs, where that pass runs (else hipErrorInvalidValue).
 hipError_t launch_permute(int T, int k, int E, int E_local, const int32_t* local_experts,
                           const int32_t* topk_idx, int32_t* offsets, int32_t* perm_token,
-                          int32_t* inv_pos, void* ws, hipStream_t st);
+                          int32_t* inv_pos, void* ws, hipStream_t st, const int32_t* src = nullptr,
+                          int S = 0, int64_t* counts = nullptr, int32_t* expert_load = nullptr);
 // x_perm[r] = x[perm_token[r]] for r < *n_rows (device scalar), capacity rows.
 hipError_t launch_gather_rows(int capacity, int H, const int32_t* perm_token,
                               const int32_t* n_rows, const uint16_t* x, uint16_t* x_perm,

@@ -23,7 +23,7 @@ int check_dims(const moe_dims* d) {
       (d->n_shared > 0 && d->I_shared < 1))
     return MOE_ERR_DIMS;
   if (d->flags < MOE_GATE_SOFTMAX_TOPK || d->flags > MOE_GATE_SIGMOID) return MOE_ERR_UNSUPPORTED;
-  if (d->E > 1024 || d->k > 32) return MOE_ERR_UNSUPPORTED;
+  if (d->E > moe::kMaxExperts || d->k > 32) return MOE_ERR_UNSUPPORTED;
   if (d->H % 8 != 0 || d->I % 8 != 0 || (d->n_shared > 0 && d->I_shared % 8 != 0))
     return MOE_ERR_UNSUPPORTED;
   if (static_cast<int64_t>(d->T) * d->k > kIntMax || static_cast<int64_t>(d->S) * d->E > kIntMax ||
@@ -412,18 +412,24 @@ int moe_forward(const moe_dims* d, const moe_gating* gating, const float* logits
     e = moe::launch_fill_i32(expert_load, d->E, 0, st);
     if (e != hipSuccess) return MOE_ERR_DEVICE;
   }
-  // decode-sized batches: the routing launch also writes the dispatch
+  // decode-sized batches: the routing launch also writes the dispatch.
+  // Larger ones are dispatched by the permute passes, whose count pass then
+  // also takes the statistics: its blocks hold many more pairs than the
+  // router's, so far fewer of their global atomic adds land on one bin.
   const moe::DispatchArgs disp{local_experts, d->E_local, offsets, perm_token, inv_pos};
+  const bool stats_in_permute = counts != nullptr && static_cast<int64_t>(d->T) * d->k > moe::kDispatchPairs;
+  int64_t* route_counts = stats_in_permute ? nullptr : counts;
   bool dispatched = false;
-  e = moe::launch_route(d->T, d->E, d->k, logits, topk_idx, topk_w, counts ? src : nullptr, d->S,
-                        counts, counts ? expert_load : nullptr, &rg, st, &disp, &dispatched);
+  e = moe::launch_route(d->T, d->E, d->k, logits, topk_idx, topk_w, route_counts ? src : nullptr, d->S,
+                        route_counts, route_counts ? expert_load : nullptr, &rg, st, &disp, &dispatched);
   if (e != hipSuccess) return MOE_ERR_DEVICE;
   record(taps, 2 * MOE_STAGE_ROUTE + 1, st);
 
   record(taps, 2 * MOE_STAGE_PERMUTE, st);
   if (!dispatched) {
-    e = moe::launch_permute(d->T, d->k, d->E, d->E_local, local_experts, topk_idx, offsets,
-                            perm_token, inv_pos, fw.permute_ws, st);
+    e = moe::launch_permute(d->T, d->k, d->E, d->E_local, local_experts, topk_idx, offsets, perm_token,
+                            inv_pos, fw.permute_ws, st, src, d->S, stats_in_permute ? counts : nullptr,
+                            stats_in_permute ? expert_load : nullptr);
     if (e != hipSuccess) return MOE_ERR_DEVICE;
   }
   // no gathered copy of x: the gate/up GEMM reads its rows through perm_token

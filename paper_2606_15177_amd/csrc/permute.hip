@@ -4,6 +4,9 @@
 // A stable counting sort of the T*k pairs by local slot, in three launches
 // over tiles of kTile consecutive pairs (token-major order):
 //   1. count   per tile and slot, LDS atomics -> tile_counts[tile][slot];
+//              in the layer's forward pass also the source x expert
+//              statistics of the tile's pairs (Sec. 5.1; over all experts),
+//              one global atomic per non-zero bin of the tile;
 //   2. scan    one block per slot: exclusive prefix over the tiles (in
 //              place) and the slot's total;
 //   3. scatter one block of kTile/64 waves per tile, a 64-pair chunk per
@@ -25,24 +28,42 @@ namespace {
 
 constexpr int kTile = kDispatchPairs;  // pairs per tile of the count and scatter passes
 
+// Optionally also the source x expert statistics of the tile's pairs (over
+// all E experts, local or not): st.counts != nullptr.
+struct PermStats {
+  int k, S;
+  const int32_t* src;
+  unsigned long long* counts;
+  int32_t* expert_load;
+  int lds_bins;  // S*E bins in LDS after the slot map and slot counts (0: global atomics)
+};
+
 __global__ __launch_bounds__(256) void perm_count_kernel(int n_pairs, int E, int E_local,
                                                          const int32_t* __restrict__ local_experts,
                                                          const int32_t* __restrict__ topk_idx,
-                                                         int32_t* __restrict__ tile_counts) {
+                                                         int32_t* __restrict__ tile_counts, PermStats st) {
   extern __shared__ int sm[];
   int* slot_of = sm;
   int* cnt = sm + E;
+  int* hist = cnt + E_local;
+  const bool stats = st.counts != nullptr;
+  const bool use_lds = st.lds_bins > 0;
   for (int s = threadIdx.x; s < E_local; s += blockDim.x) cnt[s] = 0;
-  build_slot_map(slot_of, E, E_local, local_experts);
+  if (stats && use_lds)
+    for (int b = threadIdx.x; b < st.lds_bins; b += blockDim.x) hist[b] = 0;
+  build_slot_map(slot_of, E, E_local, local_experts);  // (ends with a barrier)
   const int p0 = blockIdx.x * kTile;
   const int p1 = min(n_pairs, p0 + kTile);
   for (int p = p0 + threadIdx.x; p < p1; p += blockDim.x) {
-    const int s = slot_lookup(slot_of, topk_idx[p], E);
+    const int e = topk_idx[p];
+    const int s = slot_lookup(slot_of, e, E);
     if (s >= 0) atomicAdd(&cnt[s], 1);
+    if (stats) count_pair(st.src[p / st.k], e, st.S, E, use_lds, hist, st.counts, st.expert_load);
   }
   __syncthreads();
   for (int s = threadIdx.x; s < E_local; s += blockDim.x)
     tile_counts[static_cast<size_t>(blockIdx.x) * E_local + s] = cnt[s];
+  if (stats && use_lds) flush_hist(hist, st.lds_bins, E, st.counts, st.expert_load);
 }
 
 
@@ -161,8 +182,10 @@ size_t permute_ws_bytes(int T, int k, int E_local) {
 
 hipError_t launch_permute(int T, int k, int E, int E_local, const int32_t* local_experts,
                           const int32_t* topk_idx, int32_t* offsets, int32_t* perm_token,
-                          int32_t* inv_pos, void* ws, hipStream_t st) {
+                          int32_t* inv_pos, void* ws, hipStream_t st, const int32_t* src, int S,
+                          int64_t* counts, int32_t* expert_load) {
   const int n_pairs = T * k;
+  if (counts != nullptr && n_pairs <= kTile) return hipErrorInvalidValue;  // no count pass to take them
   if (n_pairs == 0) return launch_fill_i32(offsets, E_local + 1, 0, st);
   const int n_tiles = ceil_div(n_pairs, kTile);
   int32_t* tile_counts = static_cast<int32_t*>(ws);
@@ -172,9 +195,16 @@ hipError_t launch_permute(int T, int k, int E, int E_local, const int32_t* local
                        local_experts, topk_idx, offsets, perm_token, inv_pos);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(perm_count_kernel, dim3(n_tiles), dim3(256), lds, st, n_pairs, E, E_local,
-                     local_experts, topk_idx, tile_counts);
-  hipError_t err = hipGetLastError();
+  PermStats ps{k, S, src, reinterpret_cast<unsigned long long*>(counts), expert_load, 0};
+  if (counts != nullptr && S * E <= kLdsBinsMax) ps.lds_bins = S * E;
+  const size_t lds_count = lds + static_cast<size_t>(ps.lds_bins) * sizeof(int);
+  static unsigned long long lds_set = 0;  // devices with the LDS limit raised
+  hipError_t err = set_max_dynamic_lds(reinterpret_cast<const void*>(&perm_count_kernel),
+                                       static_cast<int>((2 * kMaxExperts + kLdsBinsMax) * sizeof(int)), &lds_set);
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(perm_count_kernel, dim3(n_tiles), dim3(256), lds_count, st, n_pairs, E, E_local,
+                     local_experts, topk_idx, tile_counts, ps);
+  err = hipGetLastError();
   if (err != hipSuccess) return err;
   int32_t* slot_total = tile_counts + static_cast<size_t>(n_tiles) * E_local;
   hipLaunchKernelGGL(perm_scan_kernel, dim3(E_local), dim3(256), 0, st, n_tiles, E_local, tile_counts, slot_total);

@@ -24,9 +24,10 @@
 // inv_pos) as the permute kernels would, saving a launch.
 //
 // Statistics (Sec. 5.1, the matrices A_{l,s,e} and B_{l,e}): each block
-// counts its pairs into an S x E int32 histogram in LDS and flushes the
-// non-zero bins with one 64-bit atomic add each.  Integer atomics make the
-// result independent of the order in which blocks land.
+// counts its pairs into an S x E histogram (see count_pair).  A route block
+// holds few tokens, so each flushes about one global atomic per pair; the
+// layer's forward pass therefore counts in the dispatch's count pass, whose
+// blocks hold 512 pairs, whenever that pass runs.
 #include "common.h"
 #include "dispatch_impl.h"
 #include "kernels.h"
@@ -35,7 +36,6 @@ namespace moe {
 namespace {
 
 constexpr int kBlock = 256;
-constexpr int kLdsBinsMax = 16384;  // S*E bins kept in LDS (64 KB)
 constexpr int kStatsPairs = 2048;   // (token, expert) pairs per block of the counting kernel
 
 __device__ __forceinline__ uint32_t order_key(float f) {
@@ -51,28 +51,6 @@ __device__ __forceinline__ float key_value(uint32_t key) {
 }
 
 __device__ __forceinline__ uint64_t umax64(uint64_t a, uint64_t b) { return a > b ? a : b; }
-
-__device__ __forceinline__ void count_pair(int s, int e, int S, int E, bool use_lds, int* hist,
-                                           unsigned long long* counts, int32_t* expert_load) {
-  if (s < 0 || s >= S || e < 0 || e >= E) return;
-  if (use_lds) {
-    atomicAdd(&hist[s * E + e], 1);
-  } else {
-    atomicAdd(&counts[static_cast<size_t>(s) * E + e], 1ull);
-    if (expert_load) atomicAdd(&expert_load[e], 1);
-  }
-}
-
-__device__ __forceinline__ void flush_hist(const int* hist, int bins, int E,
-                                           unsigned long long* counts, int32_t* expert_load) {
-  for (int b = threadIdx.x; b < bins; b += blockDim.x) {
-    const int c = hist[b];
-    if (c) {
-      atomicAdd(&counts[b], static_cast<unsigned long long>(c));
-      if (expert_load) atomicAdd(&expert_load[b % E], c);
-    }
-  }
-}
 
 struct RouteKernelArgs {
   int T, E, k, tokens_per_block;

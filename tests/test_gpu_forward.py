@@ -94,6 +94,46 @@ def test_forward_variants(moe, variant):
     assert_layer_close(res["outs"][0], ref, str(variant))
 
 
+@pytest.mark.parametrize("variant,repeat", [
+    (dict(T=600, E=64, k=4, E_local=64, S=5, src_layout="interleaved"), 2),
+    (dict(T=900, E=128, k=8, E_local=16, local_layout="choice", S=8, src_layout="blocks"), 1),
+    (dict(T=300, E=1024, k=2, E_local=40, local_layout="choice", S=17), 1),   # S*E past the LDS histogram
+])
+def test_forward_statistics_in_the_dispatch_count_pass(moe, variant, repeat):
+    """Batches of more than 512 pairs count the source x expert statistics
+    in the dispatch's count pass (over all E experts, local or not): counts
+    accumulate over calls and expert_load is set, as when the router counts."""
+    cfg = W.CONFIGS["tiny"].replace(name="stats", **variant)
+    assert cfg.T * cfg.k > 512
+    wl = W.make_workload(cfg, seed=4)
+    res = _forward(moe, cfg, wl, repeat=repeat)
+    _check_routing(cfg, wl, res, calls=repeat)
+
+
+def test_forward_statistics_skip_bad_sources(moe):
+    """Out-of-range source ids are skipped by the count pass: counts and
+    expert_load are the oracle's over the tokens with valid sources, and the
+    dispatch and output do not depend on the sources."""
+    cfg = W.CONFIGS["tiny"].replace(name="badsrc", T=700, E=32, k=3, E_local=32, S=4)
+    wl = W.make_workload(cfg, seed=6)
+    src = wl["src"].copy()
+    src[::7] = cfg.S + 3
+    src[1::11] = -1
+    wl_bad = dict(wl, src=src)
+    res = _forward(moe, cfg, wl_bad)
+    ridx, rw = oracle_route_cfg(cfg, wl)
+    np.testing.assert_array_equal(res["topk_idx"][:cfg.T], ridx)
+    ok = (src >= 0) & (src < cfg.S)
+    rc, rl = oracle.route_stats(src[ok], ridx[ok], cfg.S, cfg.E)
+    np.testing.assert_array_equal(res["counts"], rc)
+    np.testing.assert_array_equal(res["expert_load"], rl)
+    off, perm, inv = oracle.permute(ridx, cfg.E, cfg.E_local, wl["local_experts"])
+    np.testing.assert_array_equal(res["offsets"], off)
+    np.testing.assert_array_equal(res["perm_token"][: off[-1]], perm)
+    ref = oracle.forward_tokens(cfg.dims, np.arange(cfg.T), wl["logits"], wl["x"], wl["local_experts"], wl)
+    assert_layer_close(res["outs"][0], ref, "badsrc")
+
+
 def test_forward_tokens_without_local_experts(moe):
     """Tokens none of whose experts are hosted here get only the shared part;
     without shared experts they get exact zeros."""
