@@ -51,14 +51,25 @@ __global__ __launch_bounds__(256) void perm_count_kernel(int n_pairs, int E, int
   for (int s = threadIdx.x; s < E_local; s += blockDim.x) cnt[s] = 0;
   if (stats && use_lds)
     for (int b = threadIdx.x; b < st.lds_bins; b += blockDim.x) hist[b] = 0;
+  // a thread's pairs of the tile: every load goes out first, beside the
+  // slot map's (pairs past the end read pair 0 and are dropped)
+  constexpr int kPer = kTile / 256;
+  const int p0 = blockIdx.x * kTile + threadIdx.x;
+  int e[kPer], src[kPer];
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int p = p0 + i * 256;
+    const int pc = p < n_pairs ? p : 0;
+    e[i] = topk_idx[pc];
+    src[i] = stats ? st.src[pc / st.k] : 0;
+  }
   build_slot_map(slot_of, E, E_local, local_experts);  // (ends with a barrier)
-  const int p0 = blockIdx.x * kTile;
-  const int p1 = min(n_pairs, p0 + kTile);
-  for (int p = p0 + threadIdx.x; p < p1; p += blockDim.x) {
-    const int e = topk_idx[p];
-    const int s = slot_lookup(slot_of, e, E);
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    if (p0 + i * 256 >= n_pairs) break;
+    const int s = slot_lookup(slot_of, e[i], E);
     if (s >= 0) atomicAdd(&cnt[s], 1);
-    if (stats) count_pair(st.src[p / st.k], e, st.S, E, use_lds, hist, st.counts, st.expert_load);
+    if (stats) count_pair(src[i], e[i], st.S, E, use_lds, hist, st.counts, st.expert_load);
   }
   __syncthreads();
   for (int s = threadIdx.x; s < E_local; s += blockDim.x)
@@ -97,6 +108,9 @@ __global__ __launch_bounds__(kTile) void perm_scatter_kernel(
   int* cnt = base + E_local;        // [wave][slot]: chunk counts, then prefix over waves
   const int tile = blockIdx.x;
   const int wave = threadIdx.x / kWave, lane = lane_id();
+  // the pair's expert id is loaded first, beside the slot map's loads
+  const int p = tile * kTile + wave * kWave + lane;
+  const int e_p = topk_idx[p < n_pairs ? p : 0];
   for (int i = threadIdx.x; i < kScatterWaves * E_local; i += blockDim.x) cnt[i] = 0;
   build_slot_map(slot_of, E, E_local, local_experts);
   // slot offsets: exclusive scan of the totals
@@ -113,10 +127,9 @@ __global__ __launch_bounds__(kTile) void perm_scatter_kernel(
   }
   if (tile == 0 && threadIdx.x == 0) offsets[E_local] = carry;
   // rank of each pair among its chunk's pairs of the same slot
-  const int p = tile * kTile + wave * kWave + lane;
   int s = -1;
   if (p < n_pairs) {
-    s = slot_lookup(slot_of, topk_idx[p], E);
+    s = slot_lookup(slot_of, e_p, E);
     if (s < 0) inv_pos[p] = -1;
   }
   const uint64_t below = (1ull << lane) - 1ull;

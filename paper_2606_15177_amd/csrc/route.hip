@@ -150,18 +150,30 @@ __global__ __launch_bounds__(kBlock) void route_kernel(RouteKernelArgs a) {
     const bool valid = t < t1;
     uint64_t key[V];
     float lg[V];
+    // all V loads go out before the first is used: a lane past the row or
+    // the batch reads element 0 (T >= 1) and discards it, so no load sits
+    // in a branch of its own behind the previous one's wait
+    float raw[V], braw[V];
+    const bool biased = EXT && a.gate == 2 && a.bias != nullptr;
+    const int src_t = stats ? a.src[valid ? t : 0] : 0;
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+      const int e = gl + G * v;
+      raw[v] = a.logits[(valid && e < E) ? static_cast<size_t>(t) * E + e : 0];
+      braw[v] = biased ? a.bias[e < E ? e : 0] : 0.0f;
+    }
 #pragma unroll
     for (int v = 0; v < V; ++v) {
       const int e = gl + G * v;
       key[v] = 0;
       lg[v] = __builtin_nanf("");
       if (valid && e < E) {
-        const float f = a.logits[static_cast<size_t>(t) * E + e];
+        const float f = raw[v];
         lg[v] = f;
         float c = f;
         if (EXT && a.gate == 2) {
           c = sigmoid_score(f);
-          if (a.bias) c = c + a.bias[e];
+          if (biased) c = c + braw[v];
         }
         if (grouped) cval[e] = c;
         key[v] = (static_cast<uint64_t>(order_key(c)) << 32) | static_cast<uint32_t>(~e);
@@ -254,7 +266,7 @@ __global__ __launch_bounds__(kBlock) void route_kernel(RouteKernelArgs a) {
       const size_t o = static_cast<size_t>(t) * k + gl;
       a.topk_idx[o] = my_e;
       a.topk_w[o] = wgt;
-      if (stats) count_pair(a.src[t], my_e, a.S, E, use_lds, hist, a.counts, a.expert_load);
+      if (stats) count_pair(src_t, my_e, a.S, E, use_lds, hist, a.counts, a.expert_load);
     }
   }
   if (stats && use_lds) {
