@@ -184,11 +184,16 @@ __global__ __launch_bounds__(kBlock) void route_kernel(RouteKernelArgs a) {
       // between its LDS writes and reads, only the LDS wait
       __builtin_amdgcn_s_waitcnt(0xc07f);
       __builtin_amdgcn_wave_barrier();
-      // lane q: the two first selection values of expert group q, then their sum
-      uint64_t gkey = 0;
-      if (valid && gl < a.n_group) {
-        uint64_t k1 = 0, k2 = 0;
-        for (int e = gl * gsz; e < (gl + 1) * gsz; ++e) {
+      // the two first selection values of each expert group, then their sum:
+      // L lanes per group (L = G / n_group when that divides the group
+      // evenly, else 1), lane j of group q scanning elements j, j + L, ...,
+      // and the lanes' top-2 pairs merged by exchanges within the L lanes
+      const int L = (G % a.n_group == 0 && gsz % (G / a.n_group) == 0) ? G / a.n_group : 1;
+      const int q_mine = gl / L, j_mine = gl % L;
+      uint64_t k1 = 0, k2 = 0;
+      if (valid && q_mine < a.n_group) {
+        for (int i = j_mine; i < gsz; i += L) {
+          const int e = q_mine * gsz + i;
           const uint64_t ke = (static_cast<uint64_t>(order_key(cval[e])) << 32) | static_cast<uint32_t>(~e);
           if (ke > k1) {
             k2 = k1;
@@ -197,9 +202,20 @@ __global__ __launch_bounds__(kBlock) void route_kernel(RouteKernelArgs a) {
             k2 = ke;
           }
         }
+      }
+      for (int off = 1; off < L; off <<= 1) {
+        const uint64_t o1 = __shfl_xor(static_cast<unsigned long long>(k1), off);
+        const uint64_t o2 = __shfl_xor(static_cast<unsigned long long>(k2), off);
+        // top two of {k1, k2, o1, o2}; keys are distinct (the expert id is in them) or 0
+        const uint64_t hi = umax64(k1, o1), lo = k1 > o1 ? o1 : k1;
+        k2 = umax64(lo, umax64(k2, o2));
+        k1 = hi;
+      }
+      uint64_t gkey = 0;   // every lane of group q holds the group's key
+      if (valid && q_mine < a.n_group) {
         const float c1 = cval[~static_cast<uint32_t>(k1)];
         const float gs = gsz > 1 ? c1 + cval[~static_cast<uint32_t>(k2)] : c1;
-        gkey = (static_cast<uint64_t>(order_key(gs)) << 32) | static_cast<uint32_t>(~gl);
+        gkey = (static_cast<uint64_t>(order_key(gs)) << 32) | static_cast<uint32_t>(~q_mine);
       }
       uint64_t kept = 0;   // bit q: group q stays
       for (int r = 0; r < a.topk_group; ++r) {
@@ -207,7 +223,7 @@ __global__ __launch_bounds__(kBlock) void route_kernel(RouteKernelArgs a) {
         if (best == 0) break;   // a token group past the batch end
         const int q = static_cast<int>(~static_cast<uint32_t>(best));
         kept |= 1ull << q;
-        if (gl == q) gkey = 0;
+        if (q_mine == q) gkey = 0;
       }
 #pragma unroll
       for (int v = 0; v < V; ++v) {

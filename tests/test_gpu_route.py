@@ -142,6 +142,8 @@ GATED_CASES = [  # (E, k, gate, with bias, scale, n_group, topk_group)
     (8, 2, 2, True, 2.5, 4, 2), (64, 6, 2, True, 1.0, 8, 3), (256, 8, 2, True, 2.5, 8, 4),
     (256, 8, 2, False, 1.0, 0, 0), (160, 6, 2, True, 2.5, 5, 2), (1024, 16, 2, True, 1.0, 64, 8),
     (12, 3, 2, True, 1.0, 12, 3), (96, 4, 0, False, 3.0, 6, 2), (33, 5, 2, True, 1.0, 0, 0),
+    # 8 and 4 lanes of a token's lane group scan each expert group
+    (64, 4, 2, True, 1.0, 2, 1), (128, 8, 1, False, 1.0, 4, 2),
 ]
 
 
