@@ -96,31 +96,86 @@ __global__ __launch_bounds__(256) void perm_scan_kernel(int n_tiles, int E_local
 }
 
 constexpr int kScatterWaves = kTile / kWave;
+// largest tiles x slots whose counts every scatter block sums itself (64
+// KB; a thread then has at most 32 loads of 16 bytes, in batches of
+// kInlineLoads)
+constexpr int kInlineLoads = 8;
+constexpr long long kInlineScanMax = 16 * 1024;
 
+// inline_scan: tile_prefix holds the count pass's raw per-tile counts (no
+// scan pass ran); each block sums, per slot, the counts of the tiles before
+// its own and of all tiles itself (E_local a multiple of 4, at most
+// 4 kTile).  Else tile_prefix and slot_total come from the scan pass.
 __global__ __launch_bounds__(kTile) void perm_scatter_kernel(
     int n_pairs, int k, int E, int E_local, const int32_t* __restrict__ local_experts,
     const int32_t* __restrict__ topk_idx, const int32_t* __restrict__ tile_prefix,
     const int32_t* __restrict__ slot_total, int32_t* __restrict__ offsets,
-    int32_t* __restrict__ perm_token, int32_t* __restrict__ inv_pos) {
+    int32_t* __restrict__ perm_token, int32_t* __restrict__ inv_pos, bool inline_scan) {
   extern __shared__ int sm[];
   int* slot_of = sm;
   int* base = sm + E;               // first row of each slot for this tile
   int* cnt = base + E_local;        // [wave][slot]: chunk counts, then prefix over waves
+  int* part = cnt + kScatterWaves * E_local;  // inline scan: [2][rows][slot] partial sums
   const int tile = blockIdx.x;
+  const int n_tiles = ceil_div(n_pairs, kTile);
   const int wave = threadIdx.x / kWave, lane = lane_id();
   // the pair's expert id is loaded first, beside the slot map's loads
   const int p = tile * kTile + wave * kWave + lane;
   const int e_p = topk_idx[p < n_pairs ? p : 0];
   for (int i = threadIdx.x; i < kScatterWaves * E_local; i += blockDim.x) cnt[i] = 0;
-  build_slot_map(slot_of, E, E_local, local_experts);
+  if (inline_scan) {
+    // thread (row r, slots 4 sl .. 4 sl + 3) sums tiles r, r + R, ... (R
+    // rows of E_local / 4 threads), 16 bytes per load and eight loads in
+    // flight; rows then add up through LDS
+    const int W = E_local / 4;
+    const int R = kTile / W;
+    const int r = threadIdx.x / W, sl = threadIdx.x - r * W;
+    int4 before = {0, 0, 0, 0}, all = {0, 0, 0, 0};
+    if (r < R) {
+      for (int t0 = r; t0 < n_tiles; t0 += kInlineLoads * R) {
+        int4 v[kInlineLoads];
+#pragma unroll
+        for (int u = 0; u < kInlineLoads; ++u) {
+          const int tt = t0 + u * R;
+          v[u] = *reinterpret_cast<const int4*>(tile_prefix + static_cast<size_t>(tt < n_tiles ? tt : 0) * E_local +
+                                                4 * sl);
+        }
+#pragma unroll
+        for (int u = 0; u < kInlineLoads; ++u) {
+          const int tt = t0 + u * R;
+          const int4 c = tt < n_tiles ? v[u] : int4{0, 0, 0, 0};
+          all.x += c.x; all.y += c.y; all.z += c.z; all.w += c.w;
+          if (tt < tile) {
+            before.x += c.x; before.y += c.y; before.z += c.z; before.w += c.w;
+          }
+        }
+      }
+      *reinterpret_cast<int4*>(part + r * E_local + 4 * sl) = before;
+      *reinterpret_cast<int4*>(part + (R + r) * E_local + 4 * sl) = all;
+    }
+  }
+  build_slot_map(slot_of, E, E_local, local_experts);  // (ends with a barrier)
   // slot offsets: exclusive scan of the totals
   int carry = 0;
   for (int s0 = 0; s0 < E_local; s0 += blockDim.x) {
     const int s = s0 + threadIdx.x;
-    int total;
-    const int ex = block_exclusive_scan(s < E_local ? slot_total[s] : 0, &total);
+    int tot = 0, pre = 0;
     if (s < E_local) {
-      base[s] = carry + ex + tile_prefix[static_cast<size_t>(tile) * E_local + s];
+      if (inline_scan) {
+        const int R = kTile / (E_local / 4);
+        for (int r = 0; r < R; ++r) {
+          pre += part[r * E_local + s];
+          tot += part[(R + r) * E_local + s];
+        }
+      } else {
+        tot = slot_total[s];
+        pre = tile_prefix[static_cast<size_t>(tile) * E_local + s];
+      }
+    }
+    int total;
+    const int ex = block_exclusive_scan(tot, &total);
+    if (s < E_local) {
+      base[s] = carry + ex + pre;
       if (tile == 0) offsets[s] = carry + ex;
     }
     carry += total;
@@ -220,12 +275,19 @@ hipError_t launch_permute(int T, int k, int E, int E_local, const int32_t* local
   err = hipGetLastError();
   if (err != hipSuccess) return err;
   int32_t* slot_total = tile_counts + static_cast<size_t>(n_tiles) * E_local;
-  hipLaunchKernelGGL(perm_scan_kernel, dim3(E_local), dim3(256), 0, st, n_tiles, E_local, tile_counts, slot_total);
-  err = hipGetLastError();
-  if (err != hipSuccess) return err;
-  const size_t lds_scatter = static_cast<size_t>(E + (1 + kScatterWaves) * E_local) * sizeof(int);
+  // few tiles x slots: each scatter block sums the counts it needs itself,
+  // which saves the scan launch
+  const bool inline_scan = E_local % 4 == 0 && E_local <= 4 * kTile &&
+                           static_cast<long long>(n_tiles) * E_local <= kInlineScanMax;
+  if (!inline_scan) {
+    hipLaunchKernelGGL(perm_scan_kernel, dim3(E_local), dim3(256), 0, st, n_tiles, E_local, tile_counts, slot_total);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+  }
+  const size_t lds_scatter =
+      static_cast<size_t>(E + (1 + kScatterWaves) * E_local + (inline_scan ? 8 * kTile : 0)) * sizeof(int);
   hipLaunchKernelGGL(perm_scatter_kernel, dim3(n_tiles), dim3(kTile), lds_scatter, st, n_pairs, k, E, E_local,
-                     local_experts, topk_idx, tile_counts, slot_total, offsets, perm_token, inv_pos);
+                     local_experts, topk_idx, tile_counts, slot_total, offsets, perm_token, inv_pos, inline_scan);
   return hipGetLastError();
 }
 
