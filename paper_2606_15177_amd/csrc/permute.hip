@@ -97,10 +97,10 @@ __global__ __launch_bounds__(256) void perm_scan_kernel(int n_tiles, int E_local
 
 constexpr int kScatterWaves = kTile / kWave;
 // largest tiles x slots whose counts every scatter block sums itself (64
-// KB; a thread then has at most 32 loads of 16 bytes, in batches of
-// kInlineLoads)
+// KB): with four slots per 16-byte load, a thread then has at most
+// kInlineLoads loads (tiles x slots / (4 kTile)), all in flight at once
 constexpr int kInlineLoads = 8;
-constexpr long long kInlineScanMax = 16 * 1024;
+constexpr long long kInlineScanMax = 4LL * kTile * kInlineLoads;
 
 // inline_scan: tile_prefix holds the count pass's raw per-tile counts (no
 // scan pass ran); each block sums, per slot, the counts of the tiles before
@@ -125,8 +125,8 @@ __global__ __launch_bounds__(kTile) void perm_scatter_kernel(
   for (int i = threadIdx.x; i < kScatterWaves * E_local; i += blockDim.x) cnt[i] = 0;
   if (inline_scan) {
     // thread (row r, slots 4 sl .. 4 sl + 3) sums tiles r, r + R, ... (R
-    // rows of E_local / 4 threads), 16 bytes per load and eight loads in
-    // flight; rows then add up through LDS
+    // rows of E_local / 4 threads), 16 bytes per load, one batch of loads
+    // (see kInlineLoads); rows then add up through LDS
     const int W = E_local / 4;
     const int R = kTile / W;
     const int r = threadIdx.x / W, sl = threadIdx.x - r * W;
