@@ -1,8 +1,9 @@
 // Dispatch of the selected (token, expert) pairs to the locally hosted
 // experts (Sec. 2.1 dispatch; Sec. 5.2, this GPU's slice of the placement).
 //
-// A stable counting sort of the T*k pairs by local slot, in three launches
-// over tiles of kTile consecutive pairs (token-major order):
+// A stable counting sort of the T*k pairs by local slot, in three passes
+// over tiles of kTile consecutive pairs (token-major order; the second is
+// folded into the third when tiles x slots is small, see kInlineScanMax):
 //   1. count   per tile and slot, LDS atomics -> tile_counts[tile][slot];
 //              in the layer's forward pass also the source x expert
 //              statistics of the tile's pairs (Sec. 5.1; over all experts),
