@@ -74,6 +74,9 @@ def _rand_idx(rng, T, E, k):
 @pytest.mark.parametrize("T,E,k,E_local", [
     (1, 8, 2, 8), (1, 8, 2, 3), (3, 4, 4, 4), (255, 16, 2, 5), (257, 64, 6, 64), (1000, 128, 8, 17),
     (4097, 256, 8, 32), (20000, 1024, 7, 1024), (513, 1024, 32, 1),
+    # tiles x slots at and just past the bound of the scatter pass's own
+    # slot sums, one slot per 4-slot load, and 1024 slots over few tiles
+    (8192, 128, 8, 128), (8193, 128, 8, 128), (16384, 8, 2, 4), (300, 1024, 8, 1024),
 ])
 def test_permute_shapes(moe, T, E, k, E_local):
     rng = np.random.default_rng(T + E + k)
