@@ -63,14 +63,13 @@ __device__ __forceinline__ int slot_lookup(const int* slot_of, int e, int E) {
 
 // Pairs of one slot inside a 64-pair chunk, ranked by ballot + popcount
 __device__ __forceinline__ void scatter_chunk(int p, int n_pairs, int k, int E, const int* slot_of,
-                                              int* next, const int32_t* __restrict__ topk_idx,
-                                              int32_t* __restrict__ perm_token,
+                                              int* next, const int* ids, int32_t* __restrict__ perm_token,
                                               int32_t* __restrict__ inv_pos) {
   const int lane = lane_id();
   const uint64_t below = (1ull << lane) - 1ull;
   int s = -1;
   if (p < n_pairs) {
-    s = slot_lookup(slot_of, topk_idx[p], E);
+    s = slot_lookup(slot_of, ids[p], E);
     if (s < 0) inv_pos[p] = -1;
   }
   uint64_t pending = __ballot(s >= 0);
@@ -123,18 +122,19 @@ __device__ inline int block_exclusive_scan(int v, int* total) {
 
 // The whole dispatch of n_pairs pairs by one block (E_local <= blockDim.x):
 // per-slot counts, offsets [E_local + 1], then perm_token and inv_pos in
-// token order within each slot.  sm: E + E_local ints of LDS.
+// token order within each slot.  sm: E + E_local ints of LDS; ids: the
+// pairs' expert ids, already in LDS (the caller stages them; a barrier
+// must separate their writes from this call).
 __device__ inline void dispatch_one_block(int n_pairs, int k, int E, int E_local,
-                                          const int32_t* __restrict__ local_experts,
-                                          const int32_t* __restrict__ topk_idx, int32_t* __restrict__ offsets,
-                                          int32_t* __restrict__ perm_token, int32_t* __restrict__ inv_pos,
-                                          int* sm) {
+                                          const int32_t* __restrict__ local_experts, const int* ids,
+                                          int32_t* __restrict__ offsets, int32_t* __restrict__ perm_token,
+                                          int32_t* __restrict__ inv_pos, int* sm) {
   int* slot_of = sm;
   int* cnt = sm + E;  // per-slot count, then next free row
   for (int s = threadIdx.x; s < E_local; s += blockDim.x) cnt[s] = 0;
   build_slot_map(slot_of, E, E_local, local_experts);
   for (int p = threadIdx.x; p < n_pairs; p += blockDim.x) {
-    const int s = slot_lookup(slot_of, topk_idx[p], E);
+    const int s = slot_lookup(slot_of, ids[p], E);
     if (s >= 0) atomicAdd(&cnt[s], 1);
   }
   __syncthreads();
@@ -149,7 +149,7 @@ __device__ inline void dispatch_one_block(int n_pairs, int k, int E, int E_local
   __syncthreads();
   if (threadIdx.x < kWave)
     for (int c0 = 0; c0 < n_pairs; c0 += kWave)
-      scatter_chunk(c0 + threadIdx.x, n_pairs, k, E, slot_of, cnt, topk_idx, perm_token, inv_pos);
+      scatter_chunk(c0 + threadIdx.x, n_pairs, k, E, slot_of, cnt, ids, perm_token, inv_pos);
 }
 
 }  // namespace moe

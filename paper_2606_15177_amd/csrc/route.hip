@@ -139,6 +139,10 @@ __global__ __launch_bounds__(kBlock) void route_kernel(RouteKernelArgs a) {
   float* cval = reinterpret_cast<float*>(hist + a.lds_bins) + group * E;
   const bool grouped = EXT && a.n_group > 1;
   const int gsz = grouped ? E / a.n_group : E;
+  // one block routing the whole batch also dispatches it: the dispatch's
+  // tables (E + E_local ints), then the pairs' expert ids (T k ints)
+  int* disp_sm = hist + a.lds_bins + (grouped ? kGroups * E : 0);
+  int* disp_ids = disp_sm + E + a.d.E_local;
   if (stats && use_lds) {
     for (int b = tid; b < a.lds_bins; b += kBlock) hist[b] = 0;
     __syncthreads();
@@ -282,6 +286,7 @@ __global__ __launch_bounds__(kBlock) void route_kernel(RouteKernelArgs a) {
       const size_t o = static_cast<size_t>(t) * k + gl;
       a.topk_idx[o] = my_e;
       a.topk_w[o] = wgt;
+      if (a.disp) disp_ids[o] = my_e;   // (o < kDispatchPairs: one block routes the batch)
       if (stats) count_pair(src_t, my_e, a.S, E, use_lds, hist, a.counts, a.expert_load);
     }
   }
@@ -290,11 +295,10 @@ __global__ __launch_bounds__(kBlock) void route_kernel(RouteKernelArgs a) {
     flush_hist(hist, a.lds_bins, E, a.counts, a.expert_load);
   }
   if (a.disp) {
-    // this block routed the whole batch: its expert ids are in topk_idx
+    // this block routed the whole batch: its expert ids are in disp_ids
     __syncthreads();
-    int* sm = hist + a.lds_bins + (grouped ? kGroups * E : 0);
-    dispatch_one_block(T * k, k, E, a.d.E_local, a.d.local_experts, a.topk_idx, a.d.offsets, a.d.perm_token,
-                       a.d.inv_pos, sm);
+    dispatch_one_block(T * k, k, E, a.d.E_local, a.d.local_experts, disp_ids, a.d.offsets, a.d.perm_token,
+                       a.d.inv_pos, disp_sm);
   }
 }
 
@@ -341,10 +345,11 @@ hipError_t launch_route_gv(const RouteKernelArgs& in, hipStream_t st, bool* disp
   if (a.disp) a.tokens_per_block = a.T;
   a.lds_bins = (a.counts && a.S * a.E <= kLdsBinsMax) ? a.S * a.E : 0;
   const int blocks = ceil_div(a.T, a.tokens_per_block);
-  // histogram (at most 64 KB), group-limit staging (EXT), dispatch tables;
+  // histogram (at most 64 KB), group-limit staging (EXT), dispatch tables
+  // and expert ids;
   // the block-scan's partial sums take 64 more bytes of static LDS
   const size_t lds = a.lds_bins * sizeof(int) + ((EXT && a.n_group > 1) ? sizeof(float) * kGroups * a.E : 0) +
-                     (a.disp ? sizeof(int) * (a.E + a.d.E_local) : 0);
+                     (a.disp ? sizeof(int) * (a.E + a.d.E_local + kDispatchPairs) : 0);
   if (dispatched) *dispatched = a.disp;
   static unsigned long long lds_set = 0;  // devices with the LDS limit raised
   const hipError_t e_lds =
