@@ -4,6 +4,7 @@
 #pragma once
 
 #include "common.h"
+#include "kernels.h"
 
 namespace moe {
 
@@ -61,33 +62,6 @@ __device__ __forceinline__ int slot_lookup(const int* slot_of, int e, int E) {
   return (e >= 0 && e < E) ? slot_of[e] : -1;
 }
 
-// Pairs of one slot inside a 64-pair chunk, ranked by ballot + popcount
-__device__ __forceinline__ void scatter_chunk(int p, int n_pairs, int k, int E, const int* slot_of,
-                                              int* next, const int* ids, int32_t* __restrict__ perm_token,
-                                              int32_t* __restrict__ inv_pos) {
-  const int lane = lane_id();
-  const uint64_t below = (1ull << lane) - 1ull;
-  int s = -1;
-  if (p < n_pairs) {
-    s = slot_lookup(slot_of, ids[p], E);
-    if (s < 0) inv_pos[p] = -1;
-  }
-  uint64_t pending = __ballot(s >= 0);
-  while (pending) {
-    const int leader = __ffsll(static_cast<long long>(pending)) - 1;
-    const int sl = __shfl(s, leader);
-    const uint64_t same = __ballot(s == sl);
-    const int base = next[sl];
-    if (s == sl) {
-      const int pos = base + __popcll(same & below);
-      perm_token[pos] = p / k;
-      inv_pos[p] = pos;
-    }
-    if (lane == leader) next[sl] = base + __popcll(same);
-    pending &= ~same;
-  }
-}
-
 // Exclusive scan of one value per thread over a block of blockDim.x threads
 // (a multiple of 64, at most 1024).  Returns the exclusive prefix; *total
 // receives the block sum.  Ends with a barrier.
@@ -120,36 +94,90 @@ __device__ inline int block_exclusive_scan(int v, int* total) {
   return before + inc - v;
 }
 
-// The whole dispatch of n_pairs pairs by one block (E_local <= blockDim.x):
-// per-slot counts, offsets [E_local + 1], then perm_token and inv_pos in
-// token order within each slot.  sm: E + E_local ints of LDS; ids: the
-// pairs' expert ids, already in LDS (the caller stages them; a barrier
-// must separate their writes from this call).
+// LDS ints that dispatch_one_block takes: the slot map, the slot offsets and
+// the per-chunk slot counts.
+constexpr int kDispatchChunks = kDispatchPairs / kWave;
+__host__ __device__ constexpr int dispatch_one_block_ints(int E, int E_local) {
+  return E + (1 + kDispatchChunks) * E_local;
+}
+
+// The whole dispatch of n_pairs <= kDispatchPairs pairs by one block of at
+// least kDispatchPairs / 2 threads (E_local <= blockDim.x): per-slot
+// offsets [E_local + 1], then perm_token and inv_pos in token order within
+// each slot.  sm: dispatch_one_block_ints(E, E_local) ints of LDS; ids: the
+// pairs' expert ids, already in LDS (the caller stages them; a barrier must
+// separate their writes from this call).  Wave w ranks the pairs of 64-pair
+// chunks w, w + waves (at most two) by ballot + popcount, and a per-slot
+// prefix over the chunks chains them, so ties keep token order without
+// depending on atomic order.
 __device__ inline void dispatch_one_block(int n_pairs, int k, int E, int E_local,
                                           const int32_t* __restrict__ local_experts, const int* ids,
                                           int32_t* __restrict__ offsets, int32_t* __restrict__ perm_token,
                                           int32_t* __restrict__ inv_pos, int* sm) {
+  constexpr int kMaxChunksPerWave = 2;
   int* slot_of = sm;
-  int* cnt = sm + E;  // per-slot count, then next free row
-  for (int s = threadIdx.x; s < E_local; s += blockDim.x) cnt[s] = 0;
-  build_slot_map(slot_of, E, E_local, local_experts);
-  for (int p = threadIdx.x; p < n_pairs; p += blockDim.x) {
-    const int s = slot_lookup(slot_of, ids[p], E);
-    if (s >= 0) atomicAdd(&cnt[s], 1);
+  int* base = sm + E;           // per slot: total, then first row
+  int* ccnt = base + E_local;   // [chunk][slot]: chunk counts, then prefix over chunks
+  const int n_chunks = ceil_div(n_pairs, kWave);
+  const int n_waves = blockDim.x / kWave;
+  const int wave = threadIdx.x / kWave, lane = lane_id();
+  for (int i = threadIdx.x; i < n_chunks * E_local; i += blockDim.x) ccnt[i] = 0;
+  build_slot_map(slot_of, E, E_local, local_experts);  // (ends with a barrier)
+  const uint64_t below = (1ull << lane) - 1ull;
+  int slot[kMaxChunksPerWave], rank[kMaxChunksPerWave];
+#pragma unroll
+  for (int j = 0; j < kMaxChunksPerWave; ++j) {
+    const int c = wave + j * n_waves;
+    const int p = c * kWave + lane;
+    int s = -1;
+    if (c < n_chunks && p < n_pairs) {
+      s = slot_lookup(slot_of, ids[p], E);
+      if (s < 0) inv_pos[p] = -1;
+    }
+    int r = 0;
+    uint64_t pending = __ballot(s >= 0);
+    while (pending) {
+      const int leader = __ffsll(static_cast<long long>(pending)) - 1;
+      const int sl = __shfl(s, leader);
+      const uint64_t same = __ballot(s == sl);
+      if (s == sl) r = __popcll(same & below);
+      if (lane == leader) ccnt[c * E_local + sl] = __popcll(same);
+      pending &= ~same;
+    }
+    slot[j] = s;
+    rank[j] = r;
   }
   __syncthreads();
-  const int own = threadIdx.x < E_local ? cnt[threadIdx.x] : 0;
+  // per slot: prefix over the chunks, and the slot's total
+  for (int sl = threadIdx.x; sl < E_local; sl += blockDim.x) {
+    int run = 0;
+    for (int c = 0; c < n_chunks; ++c) {
+      const int v = ccnt[c * E_local + sl];
+      ccnt[c * E_local + sl] = run;
+      run += v;
+    }
+    base[sl] = run;
+  }
+  __syncthreads();
+  const int own = threadIdx.x < E_local ? base[threadIdx.x] : 0;
   int total;
-  const int excl = block_exclusive_scan(own, &total);
+  const int excl = block_exclusive_scan(own, &total);  // (ends with a barrier)
   if (threadIdx.x < E_local) {
     offsets[threadIdx.x] = excl;
-    cnt[threadIdx.x] = excl;
+    base[threadIdx.x] = excl;
   }
   if (threadIdx.x == 0) offsets[E_local] = total;
   __syncthreads();
-  if (threadIdx.x < kWave)
-    for (int c0 = 0; c0 < n_pairs; c0 += kWave)
-      scatter_chunk(c0 + threadIdx.x, n_pairs, k, E, slot_of, cnt, ids, perm_token, inv_pos);
+#pragma unroll
+  for (int j = 0; j < kMaxChunksPerWave; ++j) {
+    const int c = wave + j * n_waves;
+    const int p = c * kWave + lane;
+    if (slot[j] >= 0) {
+      const int pos = base[slot[j]] + ccnt[c * E_local + slot[j]] + rank[j];
+      perm_token[pos] = p / k;
+      inv_pos[p] = pos;
+    }
+  }
 }
 
 }  // namespace moe

@@ -225,7 +225,7 @@ __global__ __launch_bounds__(1024) void perm_single_kernel(int n_pairs, int k, i
                                                            int32_t* __restrict__ inv_pos) {
   extern __shared__ int sm[];
   // the expert ids into LDS in one pass (n_pairs <= kTile < blockDim.x)
-  int* ids = sm + E + E_local;
+  int* ids = sm + dispatch_one_block_ints(E, E_local);
   if (static_cast<int>(threadIdx.x) < n_pairs) ids[threadIdx.x] = topk_idx[threadIdx.x];
   __syncthreads();
   dispatch_one_block(n_pairs, k, E, E_local, local_experts, ids, offsets, perm_token, inv_pos, sm);
@@ -262,15 +262,15 @@ hipError_t launch_permute(int T, int k, int E, int E_local, const int32_t* local
   if (n_pairs == 0) return launch_fill_i32(offsets, E_local + 1, 0, st);
   const int n_tiles = ceil_div(n_pairs, kTile);
   int32_t* tile_counts = static_cast<int32_t*>(ws);
-  const size_t lds = static_cast<size_t>(E + E_local + kTile) * sizeof(int);
   if (n_tiles == 1) {
+    const size_t lds = static_cast<size_t>(dispatch_one_block_ints(E, E_local) + kTile) * sizeof(int);
     hipLaunchKernelGGL(perm_single_kernel, dim3(1), dim3(1024), lds, st, n_pairs, k, E, E_local,
                        local_experts, topk_idx, offsets, perm_token, inv_pos);
     return hipGetLastError();
   }
   PermStats ps{k, S, src, reinterpret_cast<unsigned long long*>(counts), expert_load, 0};
   if (counts != nullptr && S * E <= kLdsBinsMax) ps.lds_bins = S * E;
-  const size_t lds_count = lds + static_cast<size_t>(ps.lds_bins) * sizeof(int);
+  const size_t lds_count = static_cast<size_t>(E + E_local + ps.lds_bins) * sizeof(int);
   static unsigned long long lds_set = 0;  // devices with the LDS limit raised
   hipError_t err = set_max_dynamic_lds(reinterpret_cast<const void*>(&perm_count_kernel),
                                        static_cast<int>((2 * kMaxExperts + kLdsBinsMax) * sizeof(int)), &lds_set);

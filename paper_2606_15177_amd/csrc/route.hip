@@ -140,32 +140,51 @@ __global__ __launch_bounds__(kBlock) void route_kernel(RouteKernelArgs a) {
   const bool grouped = EXT && a.n_group > 1;
   const int gsz = grouped ? E / a.n_group : E;
   // one block routing the whole batch also dispatches it: the dispatch's
-  // tables (E + E_local ints), then the pairs' expert ids (T k ints)
+  // tables, then the pairs' expert ids (T k ints)
   int* disp_sm = hist + a.lds_bins + (grouped ? kGroups * E : 0);
-  int* disp_ids = disp_sm + E + a.d.E_local;
+  int* disp_ids = disp_sm + dispatch_one_block_ints(E, a.d.E_local);
   if (stats && use_lds) {
     for (int b = tid; b < a.lds_bins; b += kBlock) hist[b] = 0;
     __syncthreads();
   }
   const int t0 = blockIdx.x * a.tokens_per_block;
   const int t1 = min(T, t0 + a.tokens_per_block);
+  // The loads of a token group's pass: all V logits (and its source) go out
+  // before the first is used, and those of the block's next pass (a block
+  // that routes the whole batch makes up to four) go out before this pass
+  // computes.  A lane past the row or the batch reads element 0 (T >= 1)
+  // and discards it, so no load sits in a branch of its own behind the
+  // previous one's wait.
+  const bool biased = EXT && a.gate == 2 && a.bias != nullptr;
+  float braw[V];
+#pragma unroll
+  for (int v = 0; v < V; ++v) {
+    const int e = gl + G * v;
+    braw[v] = biased ? a.bias[e < E ? e : 0] : 0.0f;
+  }
+  float nraw[V];
+  int nsrc = 0;
+  auto load_pass = [&](int b) {
+    const int tt = b + group;
+    const bool ok = tt < t1;
+    nsrc = stats ? a.src[ok ? tt : 0] : 0;
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+      const int e = gl + G * v;
+      nraw[v] = a.logits[(ok && e < E) ? static_cast<size_t>(tt) * E + e : 0];
+    }
+  };
+  if (t0 < t1) load_pass(t0);
   for (int base = t0; base < t1; base += kGroups) {
     const int t = base + group;
     const bool valid = t < t1;
     uint64_t key[V];
     float lg[V];
-    // all V loads go out before the first is used: a lane past the row or
-    // the batch reads element 0 (T >= 1) and discards it, so no load sits
-    // in a branch of its own behind the previous one's wait
-    float raw[V], braw[V];
-    const bool biased = EXT && a.gate == 2 && a.bias != nullptr;
-    const int src_t = stats ? a.src[valid ? t : 0] : 0;
+    float raw[V];
 #pragma unroll
-    for (int v = 0; v < V; ++v) {
-      const int e = gl + G * v;
-      raw[v] = a.logits[(valid && e < E) ? static_cast<size_t>(t) * E + e : 0];
-      braw[v] = biased ? a.bias[e < E ? e : 0] : 0.0f;
-    }
+    for (int v = 0; v < V; ++v) raw[v] = nraw[v];
+    const int src_t = nsrc;
+    if (base + kGroups < t1) load_pass(base + kGroups);
 #pragma unroll
     for (int v = 0; v < V; ++v) {
       const int e = gl + G * v;
@@ -349,7 +368,7 @@ hipError_t launch_route_gv(const RouteKernelArgs& in, hipStream_t st, bool* disp
   // and expert ids;
   // the block-scan's partial sums take 64 more bytes of static LDS
   const size_t lds = a.lds_bins * sizeof(int) + ((EXT && a.n_group > 1) ? sizeof(float) * kGroups * a.E : 0) +
-                     (a.disp ? sizeof(int) * (a.E + a.d.E_local + kDispatchPairs) : 0);
+                     (a.disp ? sizeof(int) * (dispatch_one_block_ints(a.E, a.d.E_local) + kDispatchPairs) : 0);
   if (dispatched) *dispatched = a.disp;
   static unsigned long long lds_set = 0;  // devices with the LDS limit raised
   const hipError_t e_lds =
