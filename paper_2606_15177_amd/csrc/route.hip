@@ -391,9 +391,10 @@ hipError_t launch_route_g(const RouteKernelArgs& a, int V, hipStream_t st, bool*
 
 // Lanes per token G and logits per lane V: G covers E when E <= 16;
 // otherwise the narrowest G >= 16 that holds the picks (k) and the expert
-// groups (one lane each), with at most 8 logits per lane below 1024 experts.
-// Narrow groups route more tokens per wave, and a max over 16 lanes is four
-// DPP steps within a row.
+// groups (one lane each), with at most 16 logits per lane (8 for the gating
+// variants) below 1024 experts.  Narrow groups route more tokens per wave
+// (half the waves: the whole grid of a 16384-token batch resident at once),
+// and a max over 16 lanes is four DPP steps within a row.
 template <bool EXT>
 hipError_t launch_route_ext(const RouteKernelArgs& a, hipStream_t st, bool* dispatched) {
   const int E = a.E;
@@ -402,8 +403,11 @@ hipError_t launch_route_ext(const RouteKernelArgs& a, hipStream_t st, bool* disp
   if (E <= 16) {
     while (G < E) G *= 2;
   } else {
+    // at most 16 logits per lane (8 with the gating variants, whose extra
+    // state would otherwise halve the resident waves)
+    const int v_max = EXT ? 8 : 16;
     G = 16;
-    while (G < 64 && (G < need || E > 8 * G)) G *= 2;
+    while (G < 64 && (G < need || E > v_max * G)) G *= 2;
   }
   int V = 1;
   while (V * G < E) V *= 2;
