@@ -11,10 +11,11 @@
 //   2. scan    one block per slot: exclusive prefix over the tiles (in
 //              place) and the slot's total;
 //   3. scatter one block of kTile/64 waves per tile, a 64-pair chunk per
-//              wave: the pairs of one slot inside a chunk are ranked with a
-//              ballot + popcount and the chunks of a tile are chained by a
-//              per-slot prefix over the waves, so ties keep token order
-//              without depending on atomic order.  Each block also derives
+//              wave: each pair ORs its lane bit into the chunk's LDS mask
+//              of its slot and ranks itself by the popcount of the lower
+//              lanes' bits; the chunks of a tile are chained by a per-slot
+//              prefix over the waves, so ties keep token order without
+//              depending on atomic order.  Each block also derives
 //              the slot offsets from the totals (block 0 stores them).
 //              Writes perm_token and inv_pos.
 // When all pairs fit in one tile (decode-sized batches) a single one-block
@@ -113,17 +114,19 @@ __global__ __launch_bounds__(kTile) void perm_scatter_kernel(
     const int32_t* __restrict__ slot_total, int32_t* __restrict__ offsets,
     int32_t* __restrict__ perm_token, int32_t* __restrict__ inv_pos, bool inline_scan) {
   extern __shared__ int sm[];
-  int* slot_of = sm;
-  int* base = sm + E;               // first row of each slot for this tile
-  int* cnt = base + E_local;        // [wave][slot]: chunk counts, then prefix over waves
-  int* part = cnt + kScatterWaves * E_local;  // inline scan: [2][rows][slot] partial sums
+  // [wave][slot]: bit l set when lane l of the wave's chunk has the slot
+  uint64_t* mask = reinterpret_cast<uint64_t*>(sm);
+  int* part = sm + 2 * kScatterWaves * E_local;  // inline scan: [2][rows][slot] partial sums
+  int* slot_of = part + (inline_scan ? 8 * kTile : 0);
+  int* base = slot_of + E;             // first row of each slot for this tile
+  int* cnt = base + E_local;           // [wave][slot]: rows of the slot in earlier chunks
   const int tile = blockIdx.x;
   const int n_tiles = ceil_div(n_pairs, kTile);
   const int wave = threadIdx.x / kWave, lane = lane_id();
   // the pair's expert id is loaded first, beside the slot map's loads
   const int p = tile * kTile + wave * kWave + lane;
   const int e_p = topk_idx[p < n_pairs ? p : 0];
-  for (int i = threadIdx.x; i < kScatterWaves * E_local; i += blockDim.x) cnt[i] = 0;
+  for (int i = threadIdx.x; i < kScatterWaves * E_local; i += blockDim.x) mask[i] = 0;
   if (inline_scan) {
     // thread (row r, slots 4 sl .. 4 sl + 3) sums tiles r, r + R, ... (R
     // rows of E_local / 4 threads), 16 bytes per load, one batch of loads
@@ -182,34 +185,27 @@ __global__ __launch_bounds__(kTile) void perm_scatter_kernel(
     carry += total;
   }
   if (tile == 0 && threadIdx.x == 0) offsets[E_local] = carry;
-  // rank of each pair among its chunk's pairs of the same slot
+  // each pair sets its lane's bit in its chunk's mask of its slot: an OR, so
+  // the masks do not depend on the order the lanes' updates land in; a
+  // pair's rank in its chunk is then the count of lower lanes in its mask
   int s = -1;
   if (p < n_pairs) {
     s = slot_lookup(slot_of, e_p, E);
     if (s < 0) inv_pos[p] = -1;
   }
-  const uint64_t below = (1ull << lane) - 1ull;
-  int rank = 0;
-  uint64_t pending = __ballot(s >= 0);
-  while (pending) {
-    const int leader = __ffsll(static_cast<long long>(pending)) - 1;
-    const int sl = __shfl(s, leader);
-    const uint64_t same = __ballot(s == sl);
-    if (s == sl) rank = __popcll(same & below);
-    if (lane == leader) cnt[wave * E_local + sl] = __popcll(same);
-    pending &= ~same;
-  }
+  if (s >= 0) atomicOr(reinterpret_cast<unsigned long long*>(&mask[wave * E_local + s]), 1ull << lane);
   __syncthreads();
   for (int sl = threadIdx.x; sl < E_local; sl += blockDim.x) {
     int run = 0;
     for (int w = 0; w < kScatterWaves; ++w) {
-      const int c = cnt[w * E_local + sl];
       cnt[w * E_local + sl] = run;
-      run += c;
+      run += __popcll(mask[w * E_local + sl]);
     }
   }
   __syncthreads();
   if (s >= 0) {
+    const uint64_t below = (1ull << lane) - 1ull;
+    const int rank = __popcll(mask[wave * E_local + s] & below);
     const int pos = base[s] + cnt[wave * E_local + s] + rank;
     perm_token[pos] = p / k;
     inv_pos[p] = pos;
@@ -290,7 +286,13 @@ hipError_t launch_permute(int T, int k, int E, int E_local, const int32_t* local
     if (err != hipSuccess) return err;
   }
   const size_t lds_scatter =
-      static_cast<size_t>(E + (1 + kScatterWaves) * E_local + (inline_scan ? 8 * kTile : 0)) * sizeof(int);
+      static_cast<size_t>(E + (1 + 3 * kScatterWaves) * E_local + (inline_scan ? 8 * kTile : 0)) * sizeof(int);
+  static unsigned long long lds_set_scatter = 0;
+  err = set_max_dynamic_lds(reinterpret_cast<const void*>(&perm_scatter_kernel),
+                            static_cast<int>((kMaxExperts + (1 + 3 * kScatterWaves) * kMaxExperts + 8 * kTile) *
+                                             sizeof(int)),
+                            &lds_set_scatter);
+  if (err != hipSuccess) return err;
   hipLaunchKernelGGL(perm_scatter_kernel, dim3(n_tiles), dim3(kTile), lds_scatter, st, n_pairs, k, E, E_local,
                      local_experts, topk_idx, tile_counts, slot_total, offsets, perm_token, inv_pos, inline_scan);
   return hipGetLastError();
