@@ -450,7 +450,7 @@ def bench_layer(args, watch) -> int:
     # Stage breakdown from an untimed probe with an event pair around every
     # stage (ten event records cost several percent of a decode step, so the
     # timed steps carry only the dominant kernel's pair).
-    n_probe = max(3, min(args.steps, 10))
+    n_probe = max(3, min(args.steps, 20))
     ev_flags = 0 if args.fenced_events else HIP_EVENT_DISABLE_SYSTEM_FENCE
     # Probe i runs the layer twice: with the source x expert statistics
     # (events i), then without them (events n_probe + i); alternating keeps
@@ -471,10 +471,17 @@ def bench_layer(args, watch) -> int:
     # GPU time of each probe step: first stage's start to the last stage's end
     probe_steps = sorted(probe_ev.elapsed_ms(i * n_ev, i * n_ev + n_ev - 1) for i in range(n_probe))
 
-    def route_permute_ms(first):
-        return sum(probe_ev.elapsed_ms(j * n_ev, j * n_ev + 3) for j in range(first, first + n_probe)) / n_probe
-    rp_stats = route_permute_ms(0)
-    rp_no_stats = route_permute_ms(n_probe)
+    def route_permute_ms(j):
+        return probe_ev.elapsed_ms(j * n_ev, j * n_ev + 3)
+    rp_with = [route_permute_ms(i) for i in range(n_probe)]
+    rp_without = [route_permute_ms(n_probe + i) for i in range(n_probe)]
+    rp_stats = sum(rp_with) / n_probe
+    rp_no_stats = sum(rp_without) / n_probe
+    # the cost of the statistics: median over the probes of (with - without)
+    # of one probe, each pair run back to back; an event pair's own jitter of
+    # about a microsecond makes the mean of a few samples wander
+    rp_diffs = sorted(a - b for a, b in zip(rp_with, rp_without))
+    rp_overhead = rp_diffs[len(rp_diffs) // 2]
     probe_ev.close()
     dom = max(STAGES, key=lambda n: stage_ms[n])
     dom_i = STAGES.index(dom)
@@ -626,7 +633,8 @@ def bench_layer(args, watch) -> int:
                                    "min": round(probe_steps[0], 4), "samples": len(probe_steps)},
         "stats_collection": {"route_permute_ms_with_counts": round(rp_stats, 4),
                              "route_permute_ms_without_counts": round(rp_no_stats, 4),
-                             "overhead_ms": round(rp_stats - rp_no_stats, 4),
+                             "overhead_ms": round(rp_overhead, 4),
+                             "overhead_ms_of_means": round(rp_stats - rp_no_stats, 4), "samples": n_probe,
                              "counted_in": "route" if cfg.T * cfg.k <= 512 else "dispatch count pass"},
         **({"gpu_metrics": watch.stop()} if watch else {}),
         "rows_local": R,

@@ -50,10 +50,13 @@ hipError_t launch_route_stats(int T, int k, int S, int E, const int32_t* src,
 hipError_t launch_fill_i32(int32_t* p, int n, int32_t value, hipStream_t st);
 
 // ---- permute.hip -----------------------------------------------------------
-size_t permute_ws_bytes(int T, int k, int E_local);
+// Workspace of launch_permute; with S and E (the statistics' shape) it also
+// holds the count pass's per-tile histograms where those are summed in two
+// levels, and a call with counts needs the size for its S and E.
+size_t permute_ws_bytes(int T, int k, int E_local, int S = 0, int E = 0);
 // offsets / perm_token / inv_pos of the stable dispatch sort.  With counts
-// != nullptr the count pass also accumulates the source x expert counts of
-// all T*k pairs (and adds to expert_load as launch_route does); only for
+// != nullptr the launches also accumulate the source x expert counts of all
+// T*k pairs (and add to expert_load as launch_route does); only for
 // T*k > kDispatchPairs, where that pass runs (else hipErrorInvalidValue).
 hipError_t launch_permute(int T, int k, int E, int E_local, const int32_t* local_experts,
                           const int32_t* topk_idx, int32_t* offsets, int32_t* perm_token,

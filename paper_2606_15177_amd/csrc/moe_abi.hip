@@ -124,7 +124,7 @@ ForwardWs carve_forward(const moe_dims* d, void* base) {
   w.y_perm = reinterpret_cast<uint16_t*>(take(rows * d->H * sizeof(uint16_t)));
   w.y_shared = reinterpret_cast<uint16_t*>(
       take(d->n_shared > 0 ? static_cast<size_t>(d->T) * d->H * sizeof(uint16_t) : 0));
-  w.permute_ws = take(moe::permute_ws_bytes(d->T, d->k, d->E_local));
+  w.permute_ws = take(moe::permute_ws_bytes(d->T, d->k, d->E_local, d->S, d->E));
   w.ffn_ws = take(ffn_ws(d));
   w.bytes = off;
   return w;
@@ -415,7 +415,8 @@ int moe_forward(const moe_dims* d, const moe_gating* gating, const float* logits
   // decode-sized batches: the routing launch also writes the dispatch.
   // Larger ones are dispatched by the permute passes, whose count pass then
   // also takes the statistics: its blocks hold many more pairs than the
-  // router's, so far fewer of their global atomic adds land on one bin.
+  // router's, and their histograms are summed in two levels (see
+  // permute.hip) rather than by global atomics per bin and block.
   const moe::DispatchArgs disp{local_experts, d->E_local, offsets, perm_token, inv_pos};
   const bool stats_in_permute = counts != nullptr && static_cast<int64_t>(d->T) * d->k > moe::kDispatchPairs;
   int64_t* route_counts = stats_in_permute ? nullptr : counts;

@@ -6,8 +6,11 @@
 // folded into the third when tiles x slots is small, see kInlineScanMax):
 //   1. count   per tile and slot, LDS atomics -> tile_counts[tile][slot];
 //              in the layer's forward pass also the source x expert
-//              statistics of the tile's pairs (Sec. 5.1; over all experts),
-//              one global atomic per non-zero bin of the tile;
+//              statistics of the tile's pairs (Sec. 5.1; over all experts):
+//              the tile's LDS histogram is stored as one row, which extra
+//              blocks of the scatter launch sum over the tiles (one atomic
+//              per bin), or, past kStatsPartMax, flushed with one global
+//              atomic per non-zero bin of the tile;
 //   2. scan    one block per slot: exclusive prefix over the tiles (in
 //              place) and the slot's total;
 //   3. scatter one block of kTile/64 waves per tile, a 64-pair chunk per
@@ -25,6 +28,8 @@
 #include "dispatch_impl.h"
 #include "kernels.h"
 
+#include <algorithm>
+
 namespace moe {
 namespace {
 
@@ -38,7 +43,69 @@ struct PermStats {
   unsigned long long* counts;
   int32_t* expert_load;
   int lds_bins;  // S*E bins in LDS after the slot map and slot counts (0: global atomics)
+  int32_t* part;  // non-null: the tile's histogram goes to row tile of part (no atomics)
 };
+
+// Statistics summed in two levels: the count pass stores each tile's whole
+// LDS histogram as a row of part [n_tiles][S*E]; extra blocks of the
+// scatter launch, which run beside its tile blocks, each sum bpb bins (a
+// power of two) over the rows and add them to the counts with one atomic
+// per bin (and to the expert's load B).  A tile's flush instead issues one
+// global atomic per non-zero bin, and where many tiles hit the same bins
+// those atomics queue on each other.  At most kStatsLoads loads per thread
+// (bpb * n_tiles <= kStatsLoads * kTile) and kStatsPartMax ints of rows.
+constexpr int kStatsLoads = 8;
+constexpr long long kStatsPartMax = 1LL << 22;
+struct StatsReduce {
+  const int32_t* part;  // nullptr: no reduction blocks
+  int bins, bpb, E;
+  unsigned long long* counts;
+  int32_t* expert_load;
+};
+
+// Bins per reduction block, or 0 where the count pass flushes with atomics.
+int stats_bins_per_block(int n_tiles, int bins) {
+  if (n_tiles < 2 || bins <= 0 || bins > kLdsBinsMax) return 0;
+  if (static_cast<long long>(n_tiles) * bins > kStatsPartMax) return 0;
+  int bpb = 0;
+  for (int b = 1; b <= kTile && static_cast<long long>(b) * n_tiles <= static_cast<long long>(kStatsLoads) * kTile;
+       b *= 2)
+    bpb = b;
+  return bpb;
+}
+
+// One reduction block (index rb): bins rb * bpb .. + bpb - 1 of the rows.
+// Thread (row t0, bin j) sums rows t0, t0 + kTile / bpb, ...; the lanes of
+// a wave that share a bin add up by shuffles, the waves through LDS
+// (integer sums: the result does not depend on the order of the adds).
+__device__ void stats_reduce_block(const StatsReduce& sr, int n_tiles, int rb, int* red) {
+  const int bpb = sr.bpb;
+  const int j = threadIdx.x & (bpb - 1), bin = rb * bpb + j;
+  const int t0 = threadIdx.x / bpb, dt = kTile / bpb;
+  int v[kStatsLoads];
+#pragma unroll
+  for (int u = 0; u < kStatsLoads; ++u) {
+    const int t = t0 + u * dt;
+    const bool ok = t < n_tiles && bin < sr.bins;
+    v[u] = sr.part[ok ? static_cast<size_t>(t) * sr.bins + bin : 0];
+  }
+  for (int i = threadIdx.x; i < bpb; i += blockDim.x) red[i] = 0;
+  __syncthreads();
+  int c = 0;
+#pragma unroll
+  for (int u = 0; u < kStatsLoads; ++u)
+    if (t0 + u * dt < n_tiles && bin < sr.bins) c += v[u];
+  for (int off = bpb; off < kWave; off <<= 1) c += __shfl_xor(c, off);
+  if (c != 0 && (bpb >= kWave || lane_id() < bpb)) atomicAdd(&red[j], c);
+  __syncthreads();
+  if (static_cast<int>(threadIdx.x) < bpb && bin < sr.bins) {
+    const int total = red[threadIdx.x];
+    if (total != 0) {
+      atomicAdd(&sr.counts[bin], static_cast<unsigned long long>(total));
+      if (sr.expert_load) atomicAdd(&sr.expert_load[bin % sr.E], total);
+    }
+  }
+}
 
 __global__ __launch_bounds__(256) void perm_count_kernel(int n_pairs, int E, int E_local,
                                                          const int32_t* __restrict__ local_experts,
@@ -76,7 +143,14 @@ __global__ __launch_bounds__(256) void perm_count_kernel(int n_pairs, int E, int
   __syncthreads();
   for (int s = threadIdx.x; s < E_local; s += blockDim.x)
     tile_counts[static_cast<size_t>(blockIdx.x) * E_local + s] = cnt[s];
-  if (stats && use_lds) flush_hist(hist, st.lds_bins, E, st.counts, st.expert_load);
+  if (stats && use_lds) {
+    if (st.part != nullptr) {
+      int32_t* row = st.part + static_cast<size_t>(blockIdx.x) * st.lds_bins;
+      for (int b = threadIdx.x; b < st.lds_bins; b += blockDim.x) row[b] = hist[b];
+    } else {
+      flush_hist(hist, st.lds_bins, E, st.counts, st.expert_load);
+    }
+  }
 }
 
 
@@ -108,12 +182,26 @@ constexpr long long kInlineScanMax = 4LL * kTile * kInlineLoads;
 // scan pass ran); each block sums, per slot, the counts of the tiles before
 // its own and of all tiles itself (E_local a multiple of 4, at most
 // 4 kTile).  Else tile_prefix and slot_total come from the scan pass.
+// RED: blocks past the tiles sum the statistics (see StatsReduce); without
+// it the kernel has no such branch.
+template <bool RED>
 __global__ __launch_bounds__(kTile) void perm_scatter_kernel(
     int n_pairs, int k, int E, int E_local, const int32_t* __restrict__ local_experts,
     const int32_t* __restrict__ topk_idx, const int32_t* __restrict__ tile_prefix,
     const int32_t* __restrict__ slot_total, int32_t* __restrict__ offsets,
-    int32_t* __restrict__ perm_token, int32_t* __restrict__ inv_pos, bool inline_scan) {
+    int32_t* __restrict__ perm_token, int32_t* __restrict__ inv_pos, bool inline_scan, StatsReduce sr) {
   extern __shared__ int sm[];
+  if constexpr (RED) {
+    // the tile blocks' arguments are read here, before the branch on the
+    // block's role: the compiler would otherwise fetch them only past it,
+    // one more round trip to the argument segment before the first load
+    asm volatile("" ::"s"(k), "s"(E), "s"(E_local), "s"(local_experts), "s"(topk_idx), "s"(tile_prefix),
+                 "s"(slot_total), "s"(offsets), "s"(perm_token), "s"(inv_pos), "s"(static_cast<int>(inline_scan)));
+    if (static_cast<int>(blockIdx.x) >= ceil_div(n_pairs, kTile)) {
+      stats_reduce_block(sr, ceil_div(n_pairs, kTile), blockIdx.x - ceil_div(n_pairs, kTile), sm);
+      return;
+    }
+  }
   // [wave][slot]: bit l set when lane l of the wave's chunk has the slot
   uint64_t* mask = reinterpret_cast<uint64_t*>(sm);
   int* part = sm + 2 * kScatterWaves * E_local;  // inline scan: [2][rows][slot] partial sums
@@ -244,9 +332,14 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(int H, const int32_t* 
 
 }  // namespace
 
-size_t permute_ws_bytes(int T, int k, int E_local) {
-  const size_t n_tiles = static_cast<size_t>(ceil_div(T * k, kTile));
-  return (n_tiles + 1) * static_cast<size_t>(E_local) * sizeof(int32_t);  // tile counts, slot totals
+size_t permute_ws_bytes(int T, int k, int E_local, int S, int E) {
+  const int n_tiles = ceil_div(T * k, kTile);
+  // tile counts, slot totals
+  size_t bytes = (static_cast<size_t>(n_tiles) + 1) * static_cast<size_t>(E_local) * sizeof(int32_t);
+  // the statistics' per-tile rows, where they are summed in two levels
+  if (stats_bins_per_block(n_tiles, S * E) > 0)
+    bytes += static_cast<size_t>(n_tiles) * static_cast<size_t>(S * E) * sizeof(int32_t);
+  return bytes;
 }
 
 hipError_t launch_permute(int T, int k, int E, int E_local, const int32_t* local_experts,
@@ -264,8 +357,18 @@ hipError_t launch_permute(int T, int k, int E, int E_local, const int32_t* local
                        local_experts, topk_idx, offsets, perm_token, inv_pos);
     return hipGetLastError();
   }
-  PermStats ps{k, S, src, reinterpret_cast<unsigned long long*>(counts), expert_load, 0};
+  PermStats ps{k, S, src, reinterpret_cast<unsigned long long*>(counts), expert_load, 0, nullptr};
   if (counts != nullptr && S * E <= kLdsBinsMax) ps.lds_bins = S * E;
+  StatsReduce sr{nullptr, 0, 0, E, ps.counts, expert_load};
+  int n_red = 0;  // reduction blocks after the tile blocks of the scatter launch
+  if (counts != nullptr) {
+    const int bpb = stats_bins_per_block(n_tiles, S * E);
+    if (bpb > 0) {
+      ps.part = tile_counts + (static_cast<size_t>(n_tiles) + 1) * E_local;
+      sr = StatsReduce{ps.part, S * E, bpb, E, ps.counts, expert_load};
+      n_red = ceil_div(S * E, bpb);
+    }
+  }
   const size_t lds_count = static_cast<size_t>(E + E_local + ps.lds_bins) * sizeof(int);
   static unsigned long long lds_set = 0;  // devices with the LDS limit raised
   hipError_t err = set_max_dynamic_lds(reinterpret_cast<const void*>(&perm_count_kernel),
@@ -287,14 +390,23 @@ hipError_t launch_permute(int T, int k, int E, int E_local, const int32_t* local
   }
   const size_t lds_scatter =
       static_cast<size_t>(E + (1 + 3 * kScatterWaves) * E_local + (inline_scan ? 8 * kTile : 0)) * sizeof(int);
-  static unsigned long long lds_set_scatter = 0;
-  err = set_max_dynamic_lds(reinterpret_cast<const void*>(&perm_scatter_kernel),
+  static unsigned long long lds_set_scatter[2] = {0, 0};  // devices with the LDS limit raised, per variant
+  const bool red = n_red > 0;
+  err = set_max_dynamic_lds(red ? reinterpret_cast<const void*>(&perm_scatter_kernel<true>)
+                                : reinterpret_cast<const void*>(&perm_scatter_kernel<false>),
                             static_cast<int>((kMaxExperts + (1 + 3 * kScatterWaves) * kMaxExperts + 8 * kTile) *
                                              sizeof(int)),
-                            &lds_set_scatter);
+                            &lds_set_scatter[red ? 1 : 0]);
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(perm_scatter_kernel, dim3(n_tiles), dim3(kTile), lds_scatter, st, n_pairs, k, E, E_local,
-                     local_experts, topk_idx, tile_counts, slot_total, offsets, perm_token, inv_pos, inline_scan);
+  const size_t lds = std::max(lds_scatter, static_cast<size_t>(sr.bpb) * sizeof(int));
+  if (red)
+    hipLaunchKernelGGL(perm_scatter_kernel<true>, dim3(n_tiles + n_red), dim3(kTile), lds, st, n_pairs, k, E,
+                       E_local, local_experts, topk_idx, tile_counts, slot_total, offsets, perm_token, inv_pos,
+                       inline_scan, sr);
+  else
+    hipLaunchKernelGGL(perm_scatter_kernel<false>, dim3(n_tiles), dim3(kTile), lds, st, n_pairs, k, E, E_local,
+                       local_experts, topk_idx, tile_counts, slot_total, offsets, perm_token, inv_pos, inline_scan,
+                       sr);
   return hipGetLastError();
 }
 

@@ -98,11 +98,14 @@ def test_forward_variants(moe, variant):
     (dict(T=600, E=64, k=4, E_local=64, S=5, src_layout="interleaved"), 2),
     (dict(T=900, E=128, k=8, E_local=16, local_layout="choice", S=8, src_layout="blocks"), 1),
     (dict(T=300, E=1024, k=2, E_local=40, local_layout="choice", S=17), 1),   # S*E past the LDS histogram
-    # more tiles than bins (33 tiles, 32 bins), 32 tiles over 512 bins, and
-    # a 64 KB histogram in each of 4 tiles
+    # per-tile histograms summed by the scatter launch's extra blocks: more
+    # tiles than bins (33 tiles, 32 bins), 32 tiles over 512 bins, a 64 KB
+    # histogram in each of 4 tiles; and 258 tiles of 16384 bins, past the
+    # rows' limit, flushed by atomics instead
     (dict(T=4100, E=16, k=4, E_local=16, S=2), 2),
     (dict(T=2000, E=64, k=8, E_local=64, S=8), 1),
     (dict(T=200, E=1024, k=8, E_local=64, local_layout="choice", S=16), 1),
+    (dict(T=16500, E=1024, k=8, E_local=16, local_layout="choice", S=16), 2),
 ])
 def test_forward_statistics_in_the_dispatch_count_pass(moe, variant, repeat):
     """Batches of more than 512 pairs count the source x expert statistics
