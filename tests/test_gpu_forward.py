@@ -84,6 +84,10 @@ def test_forward_tiny_all_tokens_and_determinism(moe):
     dict(T=128, k=4), dict(T=129, k=2), dict(T=128, E=8, k=5),
     dict(T=32, E=256, k=8, E_local=32, local_layout="choice", S=8),
     dict(T=16, E=1024, k=8, E_local=300, local_layout="choice", S=16),   # a 64 KB statistics histogram too
+    # the largest k: routing block dispatching 512 pairs itself, and a
+    # permute-path batch whose combine sums 32 pairs per token
+    dict(T=16, E=64, k=32, E_local=64), dict(T=40, E=64, k=32, E_local=24, local_layout="choice", n_shared=1,
+                                              I_shared=64),
 ])
 def test_forward_variants(moe, variant):
     cfg = W.CONFIGS["tiny"].replace(name="variant", **variant)
