@@ -23,7 +23,10 @@
 // Two problems.  The shared experts (static rows: every token) can run in
 // the routed experts' launch: their tiles come first, and each load stream
 // and the epilogue follow the problem of the tile they are on.  This is used
-// when the shared tiles alone would leave a partly filled last round.
+// when the shared tiles alone would leave a partly filled last round.  The
+// routed experts' tail tiles (gated projection) come after them; a
+// workgroup's run of tiles then holds one problem only, so that within it
+// neither the loads nor the epilogue select a problem per tile.
 //
 // Waves.  Eight waves, two per SIMD; wave (wm, wn) owns token rows
 // 64*wm .. +63 and weight rows 128*wn .. +127 of the tile: 2 x 4
@@ -145,6 +148,11 @@ template <bool B>
 struct Half {
   static constexpr bool value = B;
 };
+// the problem of a run of full tiles: 0 (sp), 1 (g) or -1 (each tile its own)
+template <int P>
+struct Sel {
+  static constexpr int value = P;
+};
 
 // Two GEMMs of one kind in one launch: the tiles of sp (static rows, e.g. the
 // shared experts over every token; sp_tiles of them, 0 when absent) come
@@ -255,7 +263,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   auto tile_info = [&](int t_all) {
     // tile ids are wave-uniform: stated here, every branch on them is uniform
     // and so are the buffer descriptors built from the tile (else the
-    // compiler may wrap each load in a loop over the lanes' descriptors)
+    // compiler wraps each load in a loop over the lanes' descriptors)
     t_all = __builtin_amdgcn_readfirstlane(t_all);
     TileInfo ti;
     ti.tail = false;
@@ -312,6 +320,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
           ti.m0 = r * kBM;
         }
         ti.tail = __builtin_amdgcn_readfirstlane(ti.tail ? 1 : 0) != 0;
+        ti.p = 1;
         ti.g = __builtin_amdgcn_readfirstlane(ti.g);
         ti.row_base = __builtin_amdgcn_readfirstlane(ti.row_base);
         ti.m = __builtin_amdgcn_readfirstlane(ti.m);
@@ -362,7 +371,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   // first tile of its sequence past the run (loads past it are dead: no
   // traffic)
   int run_start = first, run_end = total_tiles;
-  auto prob = [&](int p) -> const GemmArgs& { return (!PAIR || p) ? a : sp; };
+  // (through ta: a selection between two captured references would index the
+  // closure at run time and keep the kernel's arguments in scratch memory)
+  auto prob = [&](int p) -> const GemmArgs& { return (!PAIR || p) ? ta.g : ta.sp; };
   const int nkb_g = ceil_div(a.K, C::BK);
   auto kmask = [&](int kb, int p, int K) { return kb * C::BK + chunk_of(p, lane) * 8 < K ? 0u : kInvalid; };
   // part P (X of stage s: 2s, W of stage s: 2s + 1) lives in slot P % 5
@@ -411,11 +422,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   // staging for it).
   // A half tile's wave (tail tiles, Half<true>) holds 2 x 2 accumulator
   // tiles: 32 output columns (gated: gate in tile 0, up in tile 1) or 64.
-  auto epilogue = [&](auto half, const TileInfo& ti, int xr0, int col_w, unsigned char* scr) {
+  auto epilogue = [&](auto half, const TileInfo& ti, const GemmArgs& pr, int xr0, int col_w, unsigned char* scr) {
     constexpr bool kHalf = decltype(half)::value;
     constexpr int kUp = kHalf ? 1 : 2;       // accumulator tile of the up rows of tile tn: tn + kUp
     constexpr int kGroups = kHalf ? 1 : 2;   // 32-column tiles (gated) or 64-column pairs (down) per wave
-    const GemmArgs& pr = prob(ti.p);
     const int ln = opaque_lane_id();
     const int erow = ln & 31, ehalf = ln >> 5;
     // The tile's output rows through a buffer descriptor: rows past the
@@ -500,7 +510,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   // of stage j - 1 takes X of stage j + 2 (among the MFMAs of stage j's
   // K-steps 1 and 2).  Before barrier j each wave waits for its loads of
   // stage j + 1; only X of stage j + 2 may still be in flight.
-  auto full_run = [&]() {
+  auto full_run = [&](auto prob_sel) {
+    // kP: the problem of every tile of the run (0: sp, 1: g), or -1 when the
+    // run takes both and each tile selects its own
+    constexpr int kP = decltype(prob_sel)::value;
+    auto pick = [&](int p) { return kP >= 0 ? kP : (PAIR ? p : 1); };
     __amdgpu_buffer_rsrc_t rs_x, rs_w;
     uint32_t xoff[C::LPP], woff[C::LPP];
     int x_tile = first, x_kb = 0, w_tile = first, w_kb = 0;
@@ -513,7 +527,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     int xr_next[C::LPP];
     auto x_rows_of = [&](int t, int (&xr)[C::LPP]) {
       const TileInfo ti = tile_info(t);
-      const GemmArgs& q = prob(PAIR ? ti.p : 1);
+      const GemmArgs& q = prob(pick(ti.p));
       const int ln = opaque_lane_id();
       if (q.x_rows) {
 #pragma unroll
@@ -528,7 +542,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       const bool live = t_in < run_end;
       const int t = live ? t_in : run_start;
       const TileInfo ti = tile_info(t);
-      x_p = PAIR ? ti.p : 1;
+      x_p = pick(ti.p);
       const GemmArgs& q = prob(x_p);
       x_nkb = PAIR ? ceil_div(q.K, C::BK) : nkb_g;
       const int ln = opaque_lane_id();
@@ -555,7 +569,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       const uint32_t dead = live ? 0u : kInvalid;
       const int t = live ? t_in : run_start;
       const TileInfo ti = tile_info(t);
-      w_p = PAIR ? ti.p : 1;
+      w_p = pick(ti.p);
       const GemmArgs& q = prob(w_p);
       w_nkb = PAIR ? ceil_div(q.K, C::BK) : nkb_g;
       const int ln = opaque_lane_id();
@@ -642,7 +656,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     int j = 0;
     for (int t = run_start; t < run_end; t += gridDim.x) {
       const TileInfo cur = tile_info(t);  // scalars, held through the K loop
-      const int nkb = PAIR ? ceil_div(prob(cur.p).K, C::BK) : nkb_g;
+      const int nkb = PAIR ? ceil_div(prob(pick(cur.p)).K, C::BK) : nkb_g;
       for (int kb = 0; kb < nkb; ++kb, ++j) {
         // K-step 0 with the second half of W of stage j + 1, K-steps 1 and 2
         // with X of stage j + 2: two loads per wave and K-step
@@ -673,7 +687,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
       }
       // the W part of the tile's last stage is free until this wave loads X
       // of the stage three ahead into its own 4 KB of it
-      epilogue(Half<false>{}, cur, xrow0, cur.nt * OUT_COLS + wn * WCOLS, part_ptr(2 * (j - 1) + 1) + wave * 4096);
+      epilogue(Half<false>{}, cur, prob(pick(cur.p)), xrow0, cur.nt * OUT_COLS + wn * WCOLS, part_ptr(2 * (j - 1) + 1) + wave * 4096);
       zero_acc();
     }
   };
@@ -808,7 +822,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         }
         // the buffer of the tile's last stage is free until the next loads
         // into it; this wave's own W rows there are its 8 KB
-        epilogue(Half<false>{}, cur, xrow0_t, cur.nt * OUT_COLS_T + wn_t * WCOLS,
+        epilogue(Half<false>{}, cur, a, xrow0_t, cur.nt * OUT_COLS_T + wn_t * WCOLS,
                  t_buf((j - 1) & 1) + T_XPART + wave * (64 * C::ROW));
         zero_acc();
       }
@@ -958,7 +972,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
         }
         // the buffer of the tile's last stage is free until the loads of the
         // stage three ahead; this wave's own W rows there are its 4 KB
-        epilogue(Half<true>{}, cur, xrow0_t, cur.nt * OUT_COLS + wn_t * (WCOLS / 2),
+        epilogue(Half<true>{}, cur, a, xrow0_t, cur.nt * OUT_COLS + wn_t * (WCOLS / 2),
                  t_buf(j - 1) + T_XPART + wave * (32 * C::ROW));
         zero_acc();
       }
@@ -970,11 +984,18 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
   // The workgroup walks its tiles t, t + gridDim, ... in runs of one kind;
   // between runs every load has landed and every wave has passed a barrier,
   // so the next run may refill the LDS from scratch.
+  // With tail tiles a run also holds tiles of one problem only (the shared
+  // problem's tiles come first and are never tails), so that its loads and
+  // epilogue select no problem per tile.
   for (int t = first; t < total_tiles;) {
     const bool tail = TAIL && tile_info(t).tail;
+    const bool shared = PAIR && t < sp_tiles;
     int e = t;
     if constexpr (TAIL) {
-      while (e < total_tiles && tile_info(e).tail == tail) e += gridDim.x;
+      if (shared)
+        e = t + ceil_div(sp_tiles - t, static_cast<int>(gridDim.x)) * static_cast<int>(gridDim.x);
+      else
+        while (e < total_tiles && tile_info(e).tail == tail) e += gridDim.x;
     } else {
       e = total_tiles;
     }
@@ -982,12 +1003,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))
     run_end = e;
     if constexpr (TAIL == 1) {
       if (tail) tail_run_wide();
-      else full_run();
+      else if (shared) full_run(Sel<0>{});
+      else full_run(Sel<1>{});
     } else if constexpr (TAIL == 2) {
       if (tail) tail_run_half();
-      else full_run();
+      else if (shared) full_run(Sel<0>{});
+      else full_run(Sel<1>{});
     } else {
-      full_run();
+      full_run(Sel<-1>{});
     }
     __builtin_amdgcn_s_waitcnt(kWaitAll);
     phase_barrier();
@@ -1034,16 +1057,21 @@ hipError_t launch_pfx(const TiledArgs& ta, long long grid, hipStream_t st) {
     }
     return launch_pfx_t<GATED, PFX, true, false, 0>(ta, grid, st);
   }
-  // (with the shared experts' tiles in the same launch the two-problem
-  // kernel keeps whole tiles: its tail variant needs more registers than
-  // two waves per SIMD allow; so does the tail variant with 16 prefix
-  // entries per lane, for more than 256 groups)
+  // (the tail variant with 16 prefix entries per lane, for more than 256
+  // groups, needs more registers than two waves per SIMD allow: there the
+  // tiles stay whole)
   if constexpr (PFX > 4) {
     return launch_pfx_t<GATED, PFX, true, false, 0>(ta, grid, st);
   } else {
-    if (ta.sp_tiles > 0) return launch_pfx_t<GATED, PFX, true, false, 0>(ta, grid, st);
-    // long K: half tail tiles, which keep pace with the full tiles of their
-    // weight rows; otherwise wide tail tiles, fewer of them (both measured)
+    // with the shared experts' tiles in the launch: half tail tiles for the
+    // gated projection, whole tiles for the down projection (where tails
+    // lost to the whole tiles); alone: on long K half tail tiles, which keep
+    // pace with the full tiles of their weight rows, otherwise wide tail
+    // tiles, fewer of them (all measured)
+    if (ta.sp_tiles > 0) {
+      if constexpr (GATED) return launch_pfx_t<GATED, PFX, true, false, 2>(ta, grid, st);
+      else return launch_pfx_t<GATED, PFX, true, false, 0>(ta, grid, st);
+    }
     if (ta.g.K >= kHalfTailK) return launch_pfx_t<GATED, PFX, false, false, 2>(ta, grid, st);
     return launch_pfx_t<GATED, PFX, false, false, 1>(ta, grid, st);
   }

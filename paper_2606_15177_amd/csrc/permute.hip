@@ -9,8 +9,9 @@
 //              statistics of the tile's pairs (Sec. 5.1; over all experts):
 //              the tile's LDS histogram is stored as one row, which extra
 //              blocks of the scatter launch sum over the tiles (one atomic
-//              per bin), or, past kStatsPartMax, flushed with one global
-//              atomic per non-zero bin of the tile;
+//              per bin), or, with too many tiles or bins for that (see
+//              stats_bins_per_block), flushed with one global atomic per
+//              non-zero bin of the tile;
 //   2. scan    one block per slot: exclusive prefix over the tiles (in
 //              place) and the slot's total;
 //   3. scatter one block of kTile/64 waves per tile, a 64-pair chunk per
